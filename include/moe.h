@@ -1,0 +1,173 @@
+/*
+ * moe.h -- C-ABI of the MI355X (gfx950) DBRX-style Mixture-of-Experts layer.
+ *
+ * The layer (Chen et al., RACS'24, "Towards Building Private LLMs: Exploring
+ * Multi-Node Expert Parallelism on Apple Silicon for Mixture-of-Experts Large
+ * Language Model"):
+ *   - Sec. 2.1: each decoder layer holds 16 FFN experts, of which the router
+ *     selects 4 per token;
+ *   - Sec. 2.2: the selected experts' outputs are combined by a weighted sum;
+ *   - Table tab:vars note (e): an expert is three D_embed x D_ffn matrices
+ *     v1, w1, w2 (here: w1 = gate with SiLU, v1 = up, w2 = down);
+ *   - Sec. 3.1 / Sec. 4.3: under expert parallelism each node holds a subset
+ *     of the experts, the router is replicated, and each node returns the
+ *     partial weighted sum of its local experts (an all-reduce adds them).
+ *   - Sec. 4.1: the weights of an expert are prestacked once into one
+ *     persistent array and indexed per layer; here moe_init takes one
+ *     caller-allocated weight arena and one workspace, and no call after it
+ *     allocates device memory.
+ *
+ * Per token t with bf16 input x[t, 0:d]:
+ *   logits[t,e] = fp32(sum_i x[t,i] * wr[i,e]) (+ bias[e], added in fp32)
+ *   S_t         = the k experts with the largest logits (ties: lower id),
+ *                 slot order = logit descending, id ascending
+ *   w[t,j]      = softmax over the k selected logits
+ *   h_j         = bf16( silu(x W1_j) * (x V1_j) )              [f]
+ *   o_j         = h_j W2_j  (fp32 accumulation)                 [d]
+ *   y[t]        = bf16( sum over local slots j of w[t,j] * o_j )
+ * The stacked form chains layers as x_next = bf16(x + y).
+ *
+ * Conventions for every entry point
+ *   - bf16 tensors are passed as uint16_t bit patterns.
+ *   - Tensor pointers are HIP device pointers unless a parameter says host;
+ *     the caller owns them.  Device tensor pointers must be 16-byte aligned.
+ *   - stream is a hipStream_t handle (NULL = the default stream).  MOE_OK
+ *     means the work was enqueued on that stream; device-side faults surface
+ *     as HIP errors at the caller's next synchronisation.
+ *   - Every argument is validated on the host before anything is launched; a
+ *     failing call enqueues nothing, returns a negative moe_status and
+ *     records a message readable through moe_last_error().  Nothing throws
+ *     or aborts across this interface.
+ *   - A context is used by one host thread and one stream at a time.
+ */
+#ifndef MOE_H
+#define MOE_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef struct moe_ctx moe_ctx;
+typedef void *moe_stream_t; /* a hipStream_t */
+
+typedef enum {
+    MOE_OK = 0,
+    MOE_E_ARG = -1,      /* null/invalid pointer or out-of-range index */
+    MOE_E_SHAPE = -2,    /* config or size not supported */
+    MOE_E_ALIGN = -3,    /* device pointer not 16-byte aligned */
+    MOE_E_CAPACITY = -4, /* T above the config's max_tokens */
+    MOE_E_STATE = -5,    /* call out of order (e.g. forward before load) */
+    MOE_E_HIP = -6       /* a HIP runtime call failed */
+} moe_status;
+
+/* Layer configuration.
+ *   d_model, ffn_dim : D_embed and D_ffn (Table tab:vars: 6144 and 10752).
+ *                      d_model must be a multiple of 256, ffn_dim of 64.
+ *   n_experts, top_k : E and k (Sec. 2.1: 16 and 4); 1 <= k <= E <= 64.
+ *   expert_begin, n_local_experts : the experts resident on this device,
+ *                      [expert_begin, expert_begin + n_local_experts).  The
+ *                      whole layer is 0, n_experts; a node's expert-parallel
+ *                      share is a sub-range (Sec. 3.1, Sec. 4.3).
+ *   n_layers         : layers held in the arena (>= 1).
+ *   max_tokens       : largest T any call will pass; sizes the workspace.
+ *   flags            : must be 0. */
+typedef struct {
+    int32_t d_model, ffn_dim, n_experts, top_k;
+    int32_t expert_begin, n_local_experts;
+    int32_t n_layers, max_tokens;
+    int32_t flags;
+} moe_config;
+
+/* Routing of the last moe_route / moe_forward call on a context.  Every
+ * pointer is a device view into the workspace, valid until the next
+ * moe_route / moe_forward / moe_forward_stack on the same context.
+ *   logits   fp32 [T, E]      topk_idx int32 [T, k]   topk_w fp32 [T, k]
+ *   counts   int32 [E]        pairs routed to each local expert (0 off-share)
+ *   offsets  int32 [E + 1]    exclusive prefix sum of counts
+ *   pair_row int32 [T, k]     row of pair (t, j) in expert-grouped order, or
+ *                             -1 when its expert is not local
+ *   row_token int32 [offsets[E]]  token of each grouped row
+ * Rows are grouped by expert ascending, then token ascending. */
+typedef struct {
+    float *logits;
+    int32_t *topk_idx;
+    float *topk_w;
+    int32_t *counts;
+    int32_t *offsets;
+    int32_t *pair_row;
+    int32_t *row_token;
+    int32_t T;
+    int32_t layer;
+} moe_routing;
+
+/* Bytes of the persistent weight arena / workspace for cfg (0 if cfg is
+ * invalid).  The arena holds, per layer, the router (fp32) and every local
+ * expert's three matrices repacked into the kernels' tiled layout. */
+size_t moe_weight_bytes(const moe_config *cfg);
+size_t moe_workspace_bytes(const moe_config *cfg);
+
+/* Validates cfg, records the caller-allocated device buffers (sizes from the
+ * functions above; they must stay allocated and unmoved until moe_destroy)
+ * and returns a new context in *out.  Allocates only the host-side context. */
+moe_status moe_init(const moe_config *cfg, void *weight_arena, void *workspace,
+                    moe_ctx **out);
+
+/* Prestacking (Sec. 4.1): repacks one local expert of one layer into the
+ * arena.  gate and up are [d, f] row-major (x gate gives the gate
+ * pre-activation), down is [f, d] row-major, all bf16.  src_on_device != 0:
+ * the three pointers are device memory and the repack is a kernel enqueued
+ * on stream; 0: they are host memory, repacked on the host and copied
+ * synchronously (the call returns after the copy).  expert is a global id
+ * inside the local range. */
+moe_status moe_load_expert(moe_ctx *ctx, int32_t layer, int32_t expert,
+                           const uint16_t *gate, const uint16_t *up,
+                           const uint16_t *down, int32_t src_on_device,
+                           moe_stream_t stream);
+
+/* Loads one layer's router: wr fp32 [d, E] row-major, bias fp32 [E] or NULL
+ * (no bias).  Same src_on_device rule as moe_load_expert. */
+moe_status moe_load_router(moe_ctx *ctx, int32_t layer, const float *wr,
+                           const float *bias, int32_t src_on_device,
+                           moe_stream_t stream);
+
+/* Router, selection and permutation for T tokens of x (bf16 [T, d]).  If
+ * logits_in (fp32 [T, E], device) is not NULL it is routed as given and the
+ * router product is skipped.  On MOE_OK, *out describes the routing (views
+ * into the workspace).  T == 0 is a no-op that reports an empty routing. */
+moe_status moe_route(moe_ctx *ctx, int32_t layer, const uint16_t *x, int32_t T,
+                     const float *logits_in, moe_routing *out,
+                     moe_stream_t stream);
+
+/* The layer: y (bf16 [T, d]) = weighted sum of the local selected experts.
+ * If r is NULL the routing is computed first (as moe_route with NULL
+ * logits_in); otherwise r must be the routing that the last moe_route on this
+ * context returned, for the same layer, x and T.  For an expert-parallel
+ * share, y is the partial sum of the local slots (zero rows for tokens with
+ * no local slot).  Requires the layer's router and local experts loaded. */
+moe_status moe_forward(moe_ctx *ctx, int32_t layer, const uint16_t *x,
+                       int32_t T, const moe_routing *r, uint16_t *y,
+                       moe_stream_t stream);
+
+/* All n_layers layers in order on T tokens, in place: for each layer l,
+ * x = bf16(x + layer_l(x)).  x_inout is bf16 [T, d]. */
+moe_status moe_forward_stack(moe_ctx *ctx, uint16_t *x_inout, int32_t T,
+                             moe_stream_t stream);
+
+/* Frees the host-side context (never the caller's device buffers). */
+void moe_destroy(moe_ctx *ctx);
+
+/* Message of the last failing call on ctx ("" if none); with ctx == NULL,
+ * the message of the last failing moe_init on this thread. */
+const char *moe_last_error(const moe_ctx *ctx);
+
+/* Static name of a status code. */
+const char *moe_status_string(moe_status s);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* MOE_H */
