@@ -50,6 +50,12 @@
 extern "C" {
 #endif
 
+#if defined(__GNUC__)
+#define MOE_API __attribute__((visibility("default")))
+#else
+#define MOE_API
+#endif
+
 typedef struct moe_ctx moe_ctx;
 typedef void *moe_stream_t; /* a hipStream_t */
 
@@ -65,7 +71,7 @@ typedef enum {
 
 /* Layer configuration.
  *   d_model, ffn_dim : D_embed and D_ffn (Table tab:vars: 6144 and 10752).
- *                      d_model must be a multiple of 256, ffn_dim of 64.
+ *                      d_model must be a multiple of 256, ffn_dim of 128.
  *   n_experts, top_k : E and k (Sec. 2.1: 16 and 4); 1 <= k <= E <= 64.
  *   expert_begin, n_local_experts : the experts resident on this device,
  *                      [expert_begin, expert_begin + n_local_experts).  The
@@ -106,13 +112,13 @@ typedef struct {
 /* Bytes of the persistent weight arena / workspace for cfg (0 if cfg is
  * invalid).  The arena holds, per layer, the router (fp32) and every local
  * expert's three matrices repacked into the kernels' tiled layout. */
-size_t moe_weight_bytes(const moe_config *cfg);
-size_t moe_workspace_bytes(const moe_config *cfg);
+MOE_API size_t moe_weight_bytes(const moe_config *cfg);
+MOE_API size_t moe_workspace_bytes(const moe_config *cfg);
 
 /* Validates cfg, records the caller-allocated device buffers (sizes from the
  * functions above; they must stay allocated and unmoved until moe_destroy)
  * and returns a new context in *out.  Allocates only the host-side context. */
-moe_status moe_init(const moe_config *cfg, void *weight_arena, void *workspace,
+MOE_API moe_status moe_init(const moe_config *cfg, void *weight_arena, void *workspace,
                     moe_ctx **out);
 
 /* Prestacking (Sec. 4.1): repacks one local expert of one layer into the
@@ -122,14 +128,14 @@ moe_status moe_init(const moe_config *cfg, void *weight_arena, void *workspace,
  * on stream; 0: they are host memory, repacked on the host and copied
  * synchronously (the call returns after the copy).  expert is a global id
  * inside the local range. */
-moe_status moe_load_expert(moe_ctx *ctx, int32_t layer, int32_t expert,
+MOE_API moe_status moe_load_expert(moe_ctx *ctx, int32_t layer, int32_t expert,
                            const uint16_t *gate, const uint16_t *up,
                            const uint16_t *down, int32_t src_on_device,
                            moe_stream_t stream);
 
 /* Loads one layer's router: wr fp32 [d, E] row-major, bias fp32 [E] or NULL
  * (no bias).  Same src_on_device rule as moe_load_expert. */
-moe_status moe_load_router(moe_ctx *ctx, int32_t layer, const float *wr,
+MOE_API moe_status moe_load_router(moe_ctx *ctx, int32_t layer, const float *wr,
                            const float *bias, int32_t src_on_device,
                            moe_stream_t stream);
 
@@ -137,7 +143,7 @@ moe_status moe_load_router(moe_ctx *ctx, int32_t layer, const float *wr,
  * logits_in (fp32 [T, E], device) is not NULL it is routed as given and the
  * router product is skipped.  On MOE_OK, *out describes the routing (views
  * into the workspace).  T == 0 is a no-op that reports an empty routing. */
-moe_status moe_route(moe_ctx *ctx, int32_t layer, const uint16_t *x, int32_t T,
+MOE_API moe_status moe_route(moe_ctx *ctx, int32_t layer, const uint16_t *x, int32_t T,
                      const float *logits_in, moe_routing *out,
                      moe_stream_t stream);
 
@@ -147,24 +153,32 @@ moe_status moe_route(moe_ctx *ctx, int32_t layer, const uint16_t *x, int32_t T,
  * context returned, for the same layer, x and T.  For an expert-parallel
  * share, y is the partial sum of the local slots (zero rows for tokens with
  * no local slot).  Requires the layer's router and local experts loaded. */
-moe_status moe_forward(moe_ctx *ctx, int32_t layer, const uint16_t *x,
+MOE_API moe_status moe_forward(moe_ctx *ctx, int32_t layer, const uint16_t *x,
                        int32_t T, const moe_routing *r, uint16_t *y,
                        moe_stream_t stream);
 
 /* All n_layers layers in order on T tokens, in place: for each layer l,
  * x = bf16(x + layer_l(x)).  x_inout is bf16 [T, d]. */
-moe_status moe_forward_stack(moe_ctx *ctx, uint16_t *x_inout, int32_t T,
+MOE_API moe_status moe_forward_stack(moe_ctx *ctx, uint16_t *x_inout, int32_t T,
                              moe_stream_t stream);
 
+/* Introspection for tests: device pointers to the intermediates of the last
+ * forward on ctx, valid until the next forward.  h: bf16 [rows, f], the
+ * SiLU-gated activations of each grouped row; o: fp32 [rows, d], each grouped
+ * row's expert output before the routing weight.  Rows follow the routing's
+ * pair_row / offsets.  Either pointer may be NULL. */
+MOE_API moe_status moe_intermediates(const moe_ctx *ctx, const uint16_t **h,
+                             const float **o);
+
 /* Frees the host-side context (never the caller's device buffers). */
-void moe_destroy(moe_ctx *ctx);
+MOE_API void moe_destroy(moe_ctx *ctx);
 
 /* Message of the last failing call on ctx ("" if none); with ctx == NULL,
  * the message of the last failing moe_init on this thread. */
-const char *moe_last_error(const moe_ctx *ctx);
+MOE_API const char *moe_last_error(const moe_ctx *ctx);
 
 /* Static name of a status code. */
-const char *moe_status_string(moe_status s);
+MOE_API const char *moe_status_string(moe_status s);
 
 #ifdef __cplusplus
 }

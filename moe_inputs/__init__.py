@@ -97,6 +97,7 @@ def _dev_lib():
     if _dev is None:
         if not os.path.exists(_DEV_LIB):
             raise RuntimeError(f"device input generator not built: {_DEV_LIB}")
+        import torch  # noqa: F401  (load torch's HIP runtime first: one runtime per process)
         lib = ctypes.CDLL(_DEV_LIB)
         for fn in (lib.moe_gen_fill_bf16_device, lib.moe_gen_fill_f32_device):
             fn.argtypes = [ctypes.c_uint32, ctypes.c_uint32, ctypes.c_uint64, ctypes.c_int64,

@@ -1,0 +1,259 @@
+"""Python binding of the gfx950 MoE library (libmoe.so, C-ABI in include/moe.h).
+
+Argument marshalling only: every step of the layer runs in the library's HIP
+kernels.  PyTorch is used for device memory and streams; if the library is not
+built this module raises on first use instead of falling back to anything.
+
+The functions carry the C names (moe_init, moe_route, moe_forward, ...).
+``MoeLayer`` bundles the caller-owned arena and workspace with a context.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+PKG_DIR = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(PKG_DIR, "libmoe.so")
+
+MOE_OK = 0
+STATUS_NAMES = {0: "MOE_OK", -1: "MOE_E_ARG", -2: "MOE_E_SHAPE", -3: "MOE_E_ALIGN",
+                -4: "MOE_E_CAPACITY", -5: "MOE_E_STATE", -6: "MOE_E_HIP"}
+
+EXPORTED = ["moe_weight_bytes", "moe_workspace_bytes", "moe_init", "moe_load_expert",
+            "moe_load_router", "moe_route", "moe_forward", "moe_forward_stack",
+            "moe_intermediates", "moe_destroy", "moe_last_error", "moe_status_string"]
+
+
+class MoeConfig(ctypes.Structure):
+    _fields_ = [("d_model", ctypes.c_int32), ("ffn_dim", ctypes.c_int32),
+                ("n_experts", ctypes.c_int32), ("top_k", ctypes.c_int32),
+                ("expert_begin", ctypes.c_int32), ("n_local_experts", ctypes.c_int32),
+                ("n_layers", ctypes.c_int32), ("max_tokens", ctypes.c_int32),
+                ("flags", ctypes.c_int32)]
+
+
+class MoeRouting(ctypes.Structure):
+    _fields_ = [("logits", ctypes.c_void_p), ("topk_idx", ctypes.c_void_p),
+                ("topk_w", ctypes.c_void_p), ("counts", ctypes.c_void_p),
+                ("offsets", ctypes.c_void_p), ("pair_row", ctypes.c_void_p),
+                ("row_token", ctypes.c_void_p), ("T", ctypes.c_int32),
+                ("layer", ctypes.c_int32)]
+
+
+class MoeError(RuntimeError):
+    def __init__(self, status: int, msg: str):
+        super().__init__(f"{STATUS_NAMES.get(status, status)}: {msg}")
+        self.status = status
+
+
+_lib = None
+
+
+def lib():
+    """The loaded libmoe.so; raises if it has not been built."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError(f"{LIB_PATH} is not built; run __graft_entry__.build()")
+        # torch first: its HIP runtime then also serves this library (one
+        # runtime per process, so torch streams are valid handles here)
+        import torch  # noqa: F401
+        L = ctypes.CDLL(LIB_PATH)
+        P, I = ctypes.c_void_p, ctypes.c_int32
+        cfgp = ctypes.POINTER(MoeConfig)
+        L.moe_weight_bytes.argtypes = [cfgp]
+        L.moe_weight_bytes.restype = ctypes.c_size_t
+        L.moe_workspace_bytes.argtypes = [cfgp]
+        L.moe_workspace_bytes.restype = ctypes.c_size_t
+        L.moe_init.argtypes = [cfgp, P, P, ctypes.POINTER(P)]
+        L.moe_load_expert.argtypes = [P, I, I, P, P, P, I, P]
+        L.moe_load_router.argtypes = [P, I, P, P, I, P]
+        L.moe_route.argtypes = [P, I, P, I, P, ctypes.POINTER(MoeRouting), P]
+        L.moe_forward.argtypes = [P, I, P, I, ctypes.POINTER(MoeRouting), P, P]
+        L.moe_forward_stack.argtypes = [P, P, I, P]
+        L.moe_intermediates.argtypes = [P, ctypes.POINTER(P), ctypes.POINTER(P)]
+        L.moe_destroy.argtypes = [P]
+        L.moe_destroy.restype = None
+        L.moe_last_error.argtypes = [P]
+        L.moe_last_error.restype = ctypes.c_char_p
+        L.moe_status_string.argtypes = [ctypes.c_int]
+        L.moe_status_string.restype = ctypes.c_char_p
+        for fn in ("moe_init", "moe_load_expert", "moe_load_router", "moe_route", "moe_forward",
+                   "moe_forward_stack", "moe_intermediates"):
+            getattr(L, fn).restype = ctypes.c_int
+        _lib = L
+    return _lib
+
+
+def _check(ctx, status: int):
+    if status != MOE_OK:
+        msg = lib().moe_last_error(ctx).decode()
+        raise MoeError(status, msg)
+
+
+def make_config(d_model, ffn_dim, n_experts, top_k, expert_begin=0, n_local_experts=0,
+                n_layers=1, max_tokens=1, flags=0) -> MoeConfig:
+    return MoeConfig(d_model, ffn_dim, n_experts, top_k, expert_begin,
+                     n_local_experts or n_experts, n_layers, max_tokens, flags)
+
+
+def moe_weight_bytes(cfg: MoeConfig) -> int:
+    return int(lib().moe_weight_bytes(ctypes.byref(cfg)))
+
+
+def moe_workspace_bytes(cfg: MoeConfig) -> int:
+    return int(lib().moe_workspace_bytes(ctypes.byref(cfg)))
+
+
+def moe_init(cfg: MoeConfig, arena_ptr: int, workspace_ptr: int) -> int:
+    out = ctypes.c_void_p()
+    _check(None, lib().moe_init(ctypes.byref(cfg), arena_ptr, workspace_ptr, ctypes.byref(out)))
+    return out.value
+
+
+def moe_load_expert(ctx, layer, expert, gate_ptr, up_ptr, down_ptr, src_on_device, stream=0):
+    _check(ctx, lib().moe_load_expert(ctx, layer, expert, gate_ptr, up_ptr, down_ptr,
+                                      src_on_device, stream))
+
+
+def moe_load_router(ctx, layer, wr_ptr, bias_ptr, src_on_device, stream=0):
+    _check(ctx, lib().moe_load_router(ctx, layer, wr_ptr, bias_ptr, src_on_device, stream))
+
+
+def moe_route(ctx, layer, x_ptr, T, logits_in_ptr=None, stream=0) -> MoeRouting:
+    r = MoeRouting()
+    _check(ctx, lib().moe_route(ctx, layer, x_ptr, T, logits_in_ptr, ctypes.byref(r), stream))
+    return r
+
+
+def moe_forward(ctx, layer, x_ptr, T, routing, y_ptr, stream=0):
+    rp = ctypes.byref(routing) if routing is not None else None
+    _check(ctx, lib().moe_forward(ctx, layer, x_ptr, T, rp, y_ptr, stream))
+
+
+def moe_forward_stack(ctx, x_ptr, T, stream=0):
+    _check(ctx, lib().moe_forward_stack(ctx, x_ptr, T, stream))
+
+
+def moe_intermediates(ctx):
+    h = ctypes.c_void_p()
+    o = ctypes.c_void_p()
+    _check(ctx, lib().moe_intermediates(ctx, ctypes.byref(h), ctypes.byref(o)))
+    return h.value, o.value
+
+
+def moe_destroy(ctx):
+    if ctx:
+        lib().moe_destroy(ctx)
+
+
+def moe_last_error(ctx) -> str:
+    return lib().moe_last_error(ctx).decode()
+
+
+# ------------------------------------------------------------ torch helper --
+
+class MoeLayer:
+    """Owns a context plus its torch-allocated arena and workspace on one GPU.
+
+    Only allocation and pointer marshalling happen here; all compute is in
+    the library."""
+
+    def __init__(self, cfg: MoeConfig, device="cuda"):
+        import torch
+        self.torch = torch
+        self.cfg = cfg
+        self.device = torch.device(device)
+        wb = moe_weight_bytes(cfg)
+        sb = moe_workspace_bytes(cfg)
+        if wb == 0 or sb == 0:
+            raise MoeError(-2, "invalid config")
+        self.arena = torch.empty(wb, dtype=torch.uint8, device=self.device)
+        self.workspace = torch.empty(sb, dtype=torch.uint8, device=self.device)
+        self.ctx = moe_init(cfg, self.arena.data_ptr(), self.workspace.data_ptr())
+
+    @property
+    def stream(self) -> int:
+        return self.torch.cuda.current_stream(self.device).cuda_stream
+
+    def close(self):
+        if getattr(self, "ctx", None):
+            moe_destroy(self.ctx)
+            self.ctx = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+    # tensors are torch tensors on self.device (bf16 as int16/uint16 views)
+    def load_expert(self, layer, expert, gate, up, down):
+        on_dev = int(gate.is_cuda)
+        moe_load_expert(self.ctx, layer, expert, gate.data_ptr(), up.data_ptr(), down.data_ptr(),
+                        on_dev, self.stream if on_dev else 0)
+
+    def load_router(self, layer, wr, bias=None):
+        on_dev = int(wr.is_cuda)
+        moe_load_router(self.ctx, layer, wr.data_ptr(), bias.data_ptr() if bias is not None else None,
+                        on_dev, self.stream if on_dev else 0)
+
+    def route(self, layer, x, T=None, logits_in=None) -> MoeRouting:
+        T = x.shape[0] if T is None else T
+        return moe_route(self.ctx, layer, x.data_ptr() if x is not None else None, T,
+                         logits_in.data_ptr() if logits_in is not None else None, self.stream)
+
+    def forward(self, layer, x, y, routing=None, T=None):
+        T = x.shape[0] if T is None else T
+        moe_forward(self.ctx, layer, x.data_ptr(), T, routing, y.data_ptr(), self.stream)
+
+    def forward_stack(self, x, T=None):
+        T = x.shape[0] if T is None else T
+        moe_forward_stack(self.ctx, x.data_ptr(), T, self.stream)
+
+    def routing_tensors(self, r: MoeRouting):
+        """Copies the routing views (device) to host numpy arrays."""
+        import numpy as np
+        torch = self.torch
+        T, E, k = r.T, self.cfg.n_experts, self.cfg.top_k
+
+        def dev(ptr, n, dtype):
+            buf = torch.empty(n, dtype=dtype, device=self.device)
+            if n:
+                _copy_dev(buf.data_ptr(), ptr, buf.numel() * buf.element_size())
+            return buf
+
+        torch.cuda.synchronize(self.device)
+        out = {
+            "logits": dev(r.logits, T * E, torch.float32).cpu().numpy().reshape(T, E),
+            "idx": dev(r.topk_idx, T * k, torch.int32).cpu().numpy().reshape(T, k),
+            "w": dev(r.topk_w, T * k, torch.float32).cpu().numpy().reshape(T, k),
+            "counts": dev(r.counts, E, torch.int32).cpu().numpy(),
+            "offsets": dev(r.offsets, E + 1, torch.int32).cpu().numpy(),
+            "pair_row": dev(r.pair_row, T * k, torch.int32).cpu().numpy().reshape(T, k),
+        }
+        n_rows = int(out["offsets"][-1])
+        out["row_token"] = dev(r.row_token, n_rows, torch.int32).cpu().numpy()
+        assert out["logits"].dtype == np.float32
+        return out
+
+
+def _copy_dev(dst_ptr: int, src_ptr: int, nbytes: int):
+    """Device-to-device copy through the HIP runtime (read-back helper)."""
+    global _hip
+    try:
+        _hip
+    except NameError:
+        # the HIP runtime already mapped into this process (torch's)
+        path = "libamdhip64.so"
+        with open(f"/proc/{os.getpid()}/maps") as fh:
+            for ln in fh:
+                if "libamdhip64" in ln and ln.split()[-1].startswith("/"):
+                    path = ln.split()[-1]
+                    break
+        _hip = ctypes.CDLL(path)
+        _hip.hipMemcpy.argtypes = [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_size_t, ctypes.c_int]
+        _hip.hipMemcpy.restype = ctypes.c_int
+    rc = _hip.hipMemcpy(ctypes.c_void_p(dst_ptr), ctypes.c_void_p(src_ptr), nbytes, 3)
+    if rc != 0:
+        raise RuntimeError(f"hipMemcpy failed: {rc}")

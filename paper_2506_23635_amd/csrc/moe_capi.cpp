@@ -1,0 +1,478 @@
+// moe_capi.cpp -- the C-ABI declared in include/moe.h: configuration checks,
+// arena and workspace carve-up, prestacking of experts, and the launch
+// sequence of one layer (router -> selection/permutation -> expert FFN ->
+// weighted combine).  No device memory is allocated here: the weight arena
+// and the workspace are the caller's (paper Sec. 4.1: weights are prestacked
+// once into a persistent array and indexed per layer).
+#include <hip/hip_runtime.h>
+
+#include <cstdio>
+#include <cstdlib>
+#include <cstring>
+#include <new>
+#include <string>
+#include <algorithm>
+#include <vector>
+
+#include "../../include/moe.h"
+#include "moe_common.h"
+
+namespace {
+
+constexpr int kDecodeMaxTokens = 16;   // token columns of one MFMA B operand
+constexpr int kMaxSlices = 64;
+constexpr size_t kAlign = 256;
+
+size_t align_up(size_t v, size_t a) { return (v + a - 1) / a * a; }
+
+struct Layout {
+    // arena
+    size_t router_bytes, bias_off, gu_bytes, dn_bytes, expert_bytes, experts_off, layer_bytes;
+    size_t arena_bytes;
+    // workspace
+    size_t partial_off, logits_off, idx_off, w_off, counts_off, offsets_off, pair_row_off,
+        row_token_off, active_off, tiles_off, n_tiles_off, h_off, o_off, ws_bytes;
+    int rows_max, max_tiles;
+};
+
+const char* check_config(const moe_config* c)
+{
+    if (!c) return "config is NULL";
+    if (c->d_model <= 0 || c->d_model % 256) return "d_model must be a positive multiple of 256";
+    if (c->ffn_dim <= 0 || c->ffn_dim % 128) return "ffn_dim must be a positive multiple of 128";
+    if (c->n_experts < 1 || c->n_experts > 64) return "n_experts must be in [1, 64]";
+    if (c->top_k < 1 || c->top_k > c->n_experts) return "top_k must be in [1, n_experts]";
+    if (c->expert_begin < 0 || c->n_local_experts < 1 ||
+        c->expert_begin + c->n_local_experts > c->n_experts)
+        return "local expert range outside [0, n_experts)";
+    if (c->n_layers < 1 || c->n_layers > 1024) return "n_layers must be in [1, 1024]";
+    if (c->max_tokens < 1 || c->max_tokens > (1 << 20)) return "max_tokens must be in [1, 2^20]";
+    if (c->flags != 0) return "flags must be 0";
+    return nullptr;
+}
+
+Layout make_layout(const moe_config* c)
+{
+    Layout L{};
+    const size_t d = c->d_model, f = c->ffn_dim, E = c->n_experts, k = c->top_k;
+    const size_t Tm = c->max_tokens, nl = c->n_local_experts;
+    L.router_bytes = align_up(d * E * 4, kAlign);
+    L.bias_off = L.router_bytes;
+    L.experts_off = L.router_bytes + align_up(E * 4, kAlign);
+    L.gu_bytes = 2 * f * d * 2;
+    L.dn_bytes = d * f * 2;
+    L.expert_bytes = L.gu_bytes + L.dn_bytes;
+    L.layer_bytes = L.experts_off + nl * L.expert_bytes;
+    L.arena_bytes = L.layer_bytes * (size_t)c->n_layers;
+
+    const size_t kl = k < nl ? k : nl;
+    L.rows_max = (int)(Tm * kl);
+    const int tile_rows = moe_prefill_tile_rows();
+    L.max_tiles = (int)((L.rows_max + tile_rows - 1) / tile_rows + nl);
+    size_t off = 0;
+    auto take = [&](size_t bytes) { size_t o = off; off = align_up(off + bytes, kAlign); return o; };
+    const size_t partial_elems = std::max((size_t)65536, Tm * E);
+    L.partial_off = take(partial_elems * 8);
+    L.logits_off = take(Tm * E * 4);
+    L.idx_off = take(Tm * k * 4);
+    L.w_off = take(Tm * k * 4);
+    L.counts_off = take(E * 4);
+    L.offsets_off = take((E + 1) * 4);
+    L.pair_row_off = take(Tm * k * 4);
+    L.row_token_off = take(Tm * k * 4);
+    L.active_off = take((E + 1) * 4);
+    L.tiles_off = take((size_t)L.max_tiles * 2 * 4);
+    L.n_tiles_off = take(4);
+    L.h_off = take((size_t)L.rows_max * f * 2);
+    L.o_off = take((size_t)L.rows_max * d * 4);
+    L.ws_bytes = off;
+    return L;
+}
+
+thread_local std::string g_init_error;
+
+}  // namespace
+
+struct moe_ctx {
+    moe_config cfg;
+    Layout L;
+    uint8_t* arena;
+    uint8_t* ws;
+    std::vector<uint8_t> router_loaded;   // [n_layers]
+    std::vector<uint8_t> has_bias;        // [n_layers]
+    std::vector<uint8_t> expert_loaded;   // [n_layers * n_local]
+    moe::RouteView rv;
+    bool gemm_lds_set;      // dynamic-LDS limit raised for the GEMM kernels
+    // last routing
+    bool route_valid;
+    int route_layer, route_T;
+    const uint16_t* route_x;
+    std::string err;
+};
+
+namespace {
+
+moe_status fail(moe_ctx* ctx, moe_status s, const std::string& msg)
+{
+    if (ctx) ctx->err = msg;
+    else g_init_error = msg;
+    return s;
+}
+
+bool misaligned(const void* p) { return ((uintptr_t)p & 15u) != 0; }
+
+moe_status hip_fail(moe_ctx* ctx, hipError_t e, const char* what)
+{
+    return fail(ctx, MOE_E_HIP, std::string(what) + ": " + hipGetErrorString(e));
+}
+
+uint8_t* layer_base(moe_ctx* c, int layer) { return c->arena + (size_t)layer * c->L.layer_bytes; }
+
+int n_slices_for(int T, int E)
+{
+    long long s = 65536LL / ((long long)T * E);
+    if (s < 1) s = 1;
+    if (s > kMaxSlices) s = kMaxSlices;
+    return (int)s;
+}
+
+moe_status check_layer(moe_ctx* ctx, int layer)
+{
+    if (layer < 0 || layer >= ctx->cfg.n_layers) return fail(ctx, MOE_E_ARG, "layer out of range");
+    if (!ctx->router_loaded[layer]) return fail(ctx, MOE_E_STATE, "router of this layer not loaded");
+    for (int i = 0; i < ctx->cfg.n_local_experts; ++i)
+        if (!ctx->expert_loaded[(size_t)layer * ctx->cfg.n_local_experts + i])
+            return fail(ctx, MOE_E_STATE, "a local expert of this layer is not loaded");
+    return MOE_OK;
+}
+
+moe_status do_route(moe_ctx* ctx, int layer, const uint16_t* x, int T, const float* logits_in,
+                    hipStream_t s)
+{
+    const moe_config& c = ctx->cfg;
+    uint8_t* lb = layer_base(ctx, layer);
+    const float* wr = reinterpret_cast<const float*>(lb);
+    const float* bias = ctx->has_bias[layer] ? reinterpret_cast<const float*>(lb + ctx->L.bias_off)
+                                             : nullptr;
+    double* partial = reinterpret_cast<double*>(ctx->ws + ctx->L.partial_off);
+    int n_slices = n_slices_for(T, c.n_experts);
+    hipError_t e;
+    if (!logits_in) {
+        e = moe_launch_router_partial(x, wr, T, c.d_model, c.n_experts, n_slices, partial, s);
+        if (e != hipSuccess) return hip_fail(ctx, e, "router kernel launch");
+    }
+    e = moe_launch_route(logits_in ? nullptr : partial, logits_in, bias, n_slices, T, c.n_experts,
+                         c.top_k, c.expert_begin, c.n_local_experts, moe_prefill_tile_rows(),
+                         &ctx->rv, s);
+    if (e != hipSuccess) return hip_fail(ctx, e, "route kernel launch");
+    ctx->route_valid = true;
+    ctx->route_layer = layer;
+    ctx->route_T = T;
+    ctx->route_x = x;
+    return MOE_OK;
+}
+
+void fill_routing(moe_ctx* ctx, int layer, int T, moe_routing* out)
+{
+    out->logits = ctx->rv.logits;
+    out->topk_idx = ctx->rv.topk_idx;
+    out->topk_w = ctx->rv.topk_w;
+    out->counts = ctx->rv.counts;
+    out->offsets = ctx->rv.offsets;
+    out->pair_row = ctx->rv.pair_row;
+    out->row_token = ctx->rv.row_token;
+    out->T = T;
+    out->layer = layer;
+}
+
+moe_status run_experts(moe_ctx* ctx, int layer, const uint16_t* x, int T, hipStream_t s)
+{
+    const moe_config& c = ctx->cfg;
+    const uint8_t* experts = layer_base(ctx, layer) + ctx->L.experts_off;
+    uint16_t* H = reinterpret_cast<uint16_t*>(ctx->ws + ctx->L.h_off);
+    float* O = reinterpret_cast<float*>(ctx->ws + ctx->L.o_off);
+    hipError_t e;
+    if (T <= kDecodeMaxTokens) {
+        moe::DecodeArgs a;
+        a.experts = experts;
+        a.expert_bytes = ctx->L.expert_bytes;
+        a.gu_bytes = ctx->L.gu_bytes;
+        a.x = x;
+        a.H = H;
+        a.O = O;
+        a.active = ctx->rv.active;
+        a.counts = ctx->rv.counts;
+        a.offsets = ctx->rv.offsets;
+        a.row_token = ctx->rv.row_token;
+        a.d = c.d_model;
+        a.f = c.ffn_dim;
+        a.e_begin = c.expert_begin;
+        int slots = std::min(c.n_local_experts, T * c.top_k);
+        e = moe_launch_decode(&a, slots, s);
+        if (e != hipSuccess) return hip_fail(ctx, e, "decode expert kernels launch");
+    } else {
+        moe::GemmArgs a;
+        a.experts = experts;
+        a.expert_bytes = ctx->L.expert_bytes;
+        a.gu_bytes = ctx->L.gu_bytes;
+        a.x = x;
+        a.H = H;
+        a.O = O;
+        a.offsets = ctx->rv.offsets;
+        a.row_token = ctx->rv.row_token;
+        a.tiles = ctx->rv.tiles;
+        a.n_tiles = ctx->rv.n_tiles;
+        a.d = c.d_model;
+        a.f = c.ffn_dim;
+        a.e_begin = c.expert_begin;
+        if (!ctx->gemm_lds_set) {
+            e = moe_prefill_set_lds_limit();
+            if (e != hipSuccess) return hip_fail(ctx, e, "GEMM kernel LDS attribute");
+            ctx->gemm_lds_set = true;
+        }
+        const int tile_rows = moe_prefill_tile_rows();
+        const int kl = std::min(c.top_k, c.n_local_experts);
+        a.max_tiles = (T * kl + tile_rows - 1) / tile_rows + c.n_local_experts;
+        e = moe_launch_prefill(&a, s);
+        if (e != hipSuccess) return hip_fail(ctx, e, "prefill expert kernels launch");
+    }
+    return MOE_OK;
+}
+
+// Host-side prestacking of one [K][N] matrix into fragment tiles.
+void pack_host(const uint16_t* src, int K, int N, uint8_t* dst, int rt_mul, int rt_add)
+{
+    const uint64_t KT = (uint64_t)K / moe::kTileK;
+    for (int n = 0; n < N; ++n) {
+        const uint64_t rt = (uint64_t)(n / moe::kTileRows) * rt_mul + rt_add;
+        for (int k0 = 0; k0 < K; k0 += 8) {
+            const uint64_t kt = (uint64_t)k0 / moe::kTileK;
+            const int lane = ((k0 % moe::kTileK) / 8) * 16 + (n % moe::kTileRows);
+            uint16_t* p = reinterpret_cast<uint16_t*>(dst + moe::tile_offset(rt, kt, KT) + lane * 16);
+            for (int i = 0; i < 8; ++i) p[i] = src[(size_t)(k0 + i) * N + n];
+        }
+    }
+}
+
+}  // namespace
+
+extern "C" {
+
+size_t moe_weight_bytes(const moe_config* cfg)
+{
+    if (check_config(cfg)) return 0;
+    return make_layout(cfg).arena_bytes;
+}
+
+size_t moe_workspace_bytes(const moe_config* cfg)
+{
+    if (check_config(cfg)) return 0;
+    return make_layout(cfg).ws_bytes;
+}
+
+moe_status moe_init(const moe_config* cfg, void* weight_arena, void* workspace, moe_ctx** out)
+{
+    if (!out) return fail(nullptr, MOE_E_ARG, "out is NULL");
+    *out = nullptr;
+    if (const char* why = check_config(cfg)) return fail(nullptr, MOE_E_SHAPE, why);
+    if (!weight_arena || !workspace) return fail(nullptr, MOE_E_ARG, "arena or workspace is NULL");
+    if (((uintptr_t)weight_arena & (kAlign - 1)) || ((uintptr_t)workspace & (kAlign - 1)))
+        return fail(nullptr, MOE_E_ALIGN, "arena and workspace must be 256-byte aligned");
+    moe_ctx* c = new (std::nothrow) moe_ctx();
+    if (!c) return fail(nullptr, MOE_E_ARG, "out of host memory");
+    c->cfg = *cfg;
+    c->L = make_layout(cfg);
+    c->arena = static_cast<uint8_t*>(weight_arena);
+    c->ws = static_cast<uint8_t*>(workspace);
+    c->router_loaded.assign(cfg->n_layers, 0);
+    c->has_bias.assign(cfg->n_layers, 0);
+    c->expert_loaded.assign((size_t)cfg->n_layers * cfg->n_local_experts, 0);
+    uint8_t* w = c->ws;
+    c->rv.logits = reinterpret_cast<float*>(w + c->L.logits_off);
+    c->rv.topk_idx = reinterpret_cast<int32_t*>(w + c->L.idx_off);
+    c->rv.topk_w = reinterpret_cast<float*>(w + c->L.w_off);
+    c->rv.counts = reinterpret_cast<int32_t*>(w + c->L.counts_off);
+    c->rv.offsets = reinterpret_cast<int32_t*>(w + c->L.offsets_off);
+    c->rv.pair_row = reinterpret_cast<int32_t*>(w + c->L.pair_row_off);
+    c->rv.row_token = reinterpret_cast<int32_t*>(w + c->L.row_token_off);
+    c->rv.active = reinterpret_cast<int32_t*>(w + c->L.active_off);
+    c->rv.tiles = reinterpret_cast<int32_t*>(w + c->L.tiles_off);
+    c->rv.n_tiles = reinterpret_cast<int32_t*>(w + c->L.n_tiles_off);
+    c->route_valid = false;
+    c->gemm_lds_set = false;
+    *out = c;
+    return MOE_OK;
+}
+
+moe_status moe_load_expert(moe_ctx* ctx, int32_t layer, int32_t expert, const uint16_t* gate,
+                           const uint16_t* up, const uint16_t* down, int32_t src_on_device,
+                           moe_stream_t stream)
+{
+    if (!ctx) return MOE_E_ARG;
+    const moe_config& c = ctx->cfg;
+    if (layer < 0 || layer >= c.n_layers) return fail(ctx, MOE_E_ARG, "layer out of range");
+    if (expert < c.expert_begin || expert >= c.expert_begin + c.n_local_experts)
+        return fail(ctx, MOE_E_ARG, "expert is not in the local range");
+    if (!gate || !up || !down) return fail(ctx, MOE_E_ARG, "weight pointer is NULL");
+    uint8_t* dst = layer_base(ctx, layer) + ctx->L.experts_off +
+                   (size_t)(expert - c.expert_begin) * ctx->L.expert_bytes;
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    const int d = c.d_model, f = c.ffn_dim;
+    if (src_on_device) {
+        if (misaligned(gate) || misaligned(up) || misaligned(down))
+            return fail(ctx, MOE_E_ALIGN, "device weight pointers must be 16-byte aligned");
+        hipError_t e;
+        if ((e = moe_launch_pack(gate, d, f, dst, 2, 0, s)) != hipSuccess ||
+            (e = moe_launch_pack(up, d, f, dst, 2, 1, s)) != hipSuccess ||
+            (e = moe_launch_pack(down, f, d, dst + ctx->L.gu_bytes, 1, 0, s)) != hipSuccess)
+            return hip_fail(ctx, e, "pack kernel launch");
+    } else {
+        std::vector<uint8_t> tmp;
+        try {
+            tmp.resize(ctx->L.expert_bytes);
+        } catch (...) {
+            return fail(ctx, MOE_E_ARG, "out of host memory for the host repack");
+        }
+        pack_host(gate, d, f, tmp.data(), 2, 0);
+        pack_host(up, d, f, tmp.data(), 2, 1);
+        pack_host(down, f, d, tmp.data() + ctx->L.gu_bytes, 1, 0);
+        hipError_t e = hipMemcpyAsync(dst, tmp.data(), tmp.size(), hipMemcpyHostToDevice, s);
+        if (e == hipSuccess) e = hipStreamSynchronize(s);
+        if (e != hipSuccess) return hip_fail(ctx, e, "host-to-device copy of packed expert");
+    }
+    ctx->expert_loaded[(size_t)layer * c.n_local_experts + (expert - c.expert_begin)] = 1;
+    return MOE_OK;
+}
+
+moe_status moe_load_router(moe_ctx* ctx, int32_t layer, const float* wr, const float* bias,
+                           int32_t src_on_device, moe_stream_t stream)
+{
+    if (!ctx) return MOE_E_ARG;
+    const moe_config& c = ctx->cfg;
+    if (layer < 0 || layer >= c.n_layers) return fail(ctx, MOE_E_ARG, "layer out of range");
+    if (!wr) return fail(ctx, MOE_E_ARG, "router weight is NULL");
+    uint8_t* lb = layer_base(ctx, layer);
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    const size_t wbytes = (size_t)c.d_model * c.n_experts * 4;
+    const hipMemcpyKind kind = src_on_device ? hipMemcpyDeviceToDevice : hipMemcpyHostToDevice;
+    hipError_t e = hipMemcpyAsync(lb, wr, wbytes, kind, s);
+    if (e == hipSuccess && bias)
+        e = hipMemcpyAsync(lb + ctx->L.bias_off, bias, (size_t)c.n_experts * 4, kind, s);
+    if (e == hipSuccess && !src_on_device) e = hipStreamSynchronize(s);
+    if (e != hipSuccess) return hip_fail(ctx, e, "router copy");
+    ctx->router_loaded[layer] = 1;
+    ctx->has_bias[layer] = bias ? 1 : 0;
+    return MOE_OK;
+}
+
+moe_status moe_route(moe_ctx* ctx, int32_t layer, const uint16_t* x, int32_t T,
+                     const float* logits_in, moe_routing* out, moe_stream_t stream)
+{
+    if (!ctx) return MOE_E_ARG;
+    if (!out) return fail(ctx, MOE_E_ARG, "out is NULL");
+    if (layer < 0 || layer >= ctx->cfg.n_layers) return fail(ctx, MOE_E_ARG, "layer out of range");
+    if (T < 0) return fail(ctx, MOE_E_ARG, "T is negative");
+    if (T > ctx->cfg.max_tokens) return fail(ctx, MOE_E_CAPACITY, "T exceeds max_tokens");
+    if (!ctx->router_loaded[layer]) return fail(ctx, MOE_E_STATE, "router of this layer not loaded");
+    ctx->route_valid = false;
+    if (T == 0) {
+        fill_routing(ctx, layer, 0, out);
+        return MOE_OK;
+    }
+    if (!logits_in) {
+        if (!x) return fail(ctx, MOE_E_ARG, "x is NULL");
+        if (misaligned(x)) return fail(ctx, MOE_E_ALIGN, "x must be 16-byte aligned");
+    } else if (misaligned(logits_in)) {
+        return fail(ctx, MOE_E_ALIGN, "logits_in must be 16-byte aligned");
+    }
+    moe_status st = do_route(ctx, layer, x, T, logits_in, static_cast<hipStream_t>(stream));
+    if (st != MOE_OK) return st;
+    fill_routing(ctx, layer, T, out);
+    return MOE_OK;
+}
+
+moe_status moe_forward(moe_ctx* ctx, int32_t layer, const uint16_t* x, int32_t T,
+                       const moe_routing* r, uint16_t* y, moe_stream_t stream)
+{
+    if (!ctx) return MOE_E_ARG;
+    if (T < 0) return fail(ctx, MOE_E_ARG, "T is negative");
+    if (T > ctx->cfg.max_tokens) return fail(ctx, MOE_E_CAPACITY, "T exceeds max_tokens");
+    moe_status st = check_layer(ctx, layer);
+    if (st != MOE_OK) return st;
+    if (T == 0) return MOE_OK;
+    if (!x || !y) return fail(ctx, MOE_E_ARG, "x or y is NULL");
+    if (misaligned(x) || misaligned(y)) return fail(ctx, MOE_E_ALIGN, "x and y must be 16-byte aligned");
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    if (r) {
+        if (!ctx->route_valid || r->T != T || r->layer != layer || r->logits != ctx->rv.logits ||
+            ctx->route_T != T || ctx->route_layer != layer)
+            return fail(ctx, MOE_E_STATE, "routing does not belong to the last moe_route of this layer and T");
+    } else {
+        st = do_route(ctx, layer, x, T, nullptr, s);
+        if (st != MOE_OK) return st;
+    }
+    st = run_experts(ctx, layer, x, T, s);
+    if (st != MOE_OK) return st;
+    hipError_t e = moe_launch_combine(reinterpret_cast<const float*>(ctx->ws + ctx->L.o_off),
+                                      ctx->rv.pair_row, ctx->rv.topk_w, T, ctx->cfg.d_model,
+                                      ctx->cfg.top_k, y, nullptr, s);
+    if (e != hipSuccess) return hip_fail(ctx, e, "combine kernel launch");
+    return MOE_OK;
+}
+
+moe_status moe_forward_stack(moe_ctx* ctx, uint16_t* x_inout, int32_t T, moe_stream_t stream)
+{
+    if (!ctx) return MOE_E_ARG;
+    if (T < 0) return fail(ctx, MOE_E_ARG, "T is negative");
+    if (T > ctx->cfg.max_tokens) return fail(ctx, MOE_E_CAPACITY, "T exceeds max_tokens");
+    for (int l = 0; l < ctx->cfg.n_layers; ++l) {
+        moe_status st = check_layer(ctx, l);
+        if (st != MOE_OK) return st;
+    }
+    if (T == 0) return MOE_OK;
+    if (!x_inout) return fail(ctx, MOE_E_ARG, "x is NULL");
+    if (misaligned(x_inout)) return fail(ctx, MOE_E_ALIGN, "x must be 16-byte aligned");
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    for (int l = 0; l < ctx->cfg.n_layers; ++l) {
+        moe_status st = do_route(ctx, l, x_inout, T, nullptr, s);
+        if (st != MOE_OK) return st;
+        st = run_experts(ctx, l, x_inout, T, s);
+        if (st != MOE_OK) return st;
+        hipError_t e = moe_launch_combine(reinterpret_cast<const float*>(ctx->ws + ctx->L.o_off),
+                                          ctx->rv.pair_row, ctx->rv.topk_w, T, ctx->cfg.d_model,
+                                          ctx->cfg.top_k, nullptr, x_inout, s);
+        if (e != hipSuccess) return hip_fail(ctx, e, "combine kernel launch");
+    }
+    return MOE_OK;
+}
+
+moe_status moe_intermediates(const moe_ctx* ctx, const uint16_t** h, const float** o)
+{
+    if (!ctx) return MOE_E_ARG;
+    if (h) *h = reinterpret_cast<const uint16_t*>(ctx->ws + ctx->L.h_off);
+    if (o) *o = reinterpret_cast<const float*>(ctx->ws + ctx->L.o_off);
+    return MOE_OK;
+}
+
+void moe_destroy(moe_ctx* ctx) { delete ctx; }
+
+const char* moe_last_error(const moe_ctx* ctx)
+{
+    return ctx ? ctx->err.c_str() : g_init_error.c_str();
+}
+
+const char* moe_status_string(moe_status s)
+{
+    switch (s) {
+    case MOE_OK: return "MOE_OK";
+    case MOE_E_ARG: return "MOE_E_ARG";
+    case MOE_E_SHAPE: return "MOE_E_SHAPE";
+    case MOE_E_ALIGN: return "MOE_E_ALIGN";
+    case MOE_E_CAPACITY: return "MOE_E_CAPACITY";
+    case MOE_E_STATE: return "MOE_E_STATE";
+    case MOE_E_HIP: return "MOE_E_HIP";
+    }
+    return "unknown";
+}
+
+}  // extern "C"

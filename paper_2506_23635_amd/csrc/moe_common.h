@@ -1,0 +1,162 @@
+// moe_common.h -- shared device helpers and the packed weight layout of the
+// gfx950 MoE library.
+//
+// Packed ("fragment-tiled") weight layout
+// ---------------------------------------
+// Every expert matrix is stored with its output features as rows and its
+// reduction dimension K contiguous, cut into 16-row x 32-K tiles of 1 KiB.
+// Inside a tile, 16-byte granule g (0..63) holds the 8 consecutive K values
+// k = 8*(g/16) .. 8*(g/16)+7 of row g%16, which is exactly the bf16 operand a
+// lane of a wave supplies to v_mfma_f32_16x16x32_bf16 (lane l: row l%16,
+// K-group l/16).  A row tile's K tiles are consecutive, so a 16-row slab is
+// one contiguous run and every wave-wide 16-byte load is 1 KiB contiguous.
+//
+//   GU (gate+up)  : 2*f rows x d K. Row tile 2b holds gate (w1) features
+//                   16b..16b+15, row tile 2b+1 the up (v1) features of the
+//                   same indices, so one wave owns both halves of a SiLU pair.
+//   DN (down)     : d rows x f K, row tile q holds output features 16q..16q+15.
+//
+// Arena per layer: router wr fp32 [d,E] | bias fp32 [E] (padded) | for each
+// local expert: GU then DN.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace moe {
+
+typedef __attribute__((__vector_size__(8 * sizeof(__bf16)))) __bf16 bf16x8_t;
+typedef __attribute__((__vector_size__(4 * sizeof(float)))) float f32x4_t;
+typedef __attribute__((__vector_size__(4 * sizeof(uint32_t)))) uint32_t u32x4_t;
+
+constexpr int kTileRows = 16;
+constexpr int kTileK = 32;
+constexpr int kTileBytes = kTileRows * kTileK * 2;  // 1 KiB
+constexpr int kWave = 64;
+
+// Byte offset of (row tile rt, K tile kt) for a matrix with KT K tiles.
+__host__ __device__ inline uint64_t tile_offset(uint64_t rt, uint64_t kt, uint64_t KT)
+{
+    return (rt * KT + kt) * (uint64_t)kTileBytes;
+}
+
+__device__ inline float bf16_to_f32(uint16_t b)
+{
+    return __uint_as_float((uint32_t)b << 16);
+}
+
+// fp32 -> bf16, round to nearest even (inputs here are finite).
+__device__ inline uint16_t f32_to_bf16(float v)
+{
+    uint32_t u = __float_as_uint(v);
+    if ((u & 0x7F800000u) == 0x7F800000u)  // inf / nan: keep, quiet the nan
+        return (uint16_t)((u >> 16) | ((u & 0x007FFFFFu) ? 0x40u : 0u));
+    u += 0x7FFFu + ((u >> 16) & 1u);
+    return (uint16_t)(u >> 16);
+}
+
+// fp64 -> bf16, one rounding to nearest even, integer arithmetic on the bits.
+__device__ inline uint16_t f64_to_bf16(double v)
+{
+    uint64_t b = (uint64_t)__double_as_longlong(v);
+    uint16_t sign = (uint16_t)((b >> 48) & 0x8000u);
+    uint64_t a = b & 0x7FFFFFFFFFFFFFFFull;
+    if (a >= 0x7FF0000000000000ull)
+        return (uint16_t)(sign | (a == 0x7FF0000000000000ull ? 0x7F80u : 0x7FC0u));
+    int bexp = (int)(a >> 52);
+    if (bexp == 0)
+        return sign;
+    uint64_t mant = (a & 0x000FFFFFFFFFFFFFull) | 0x0010000000000000ull;
+    int e = bexp - 1023;
+    int qexp = (e < -126 ? -126 : e) - 7;
+    int shift = qexp - (bexp - 1075);
+    if (shift > 54)
+        return sign;
+    uint64_t q = mant >> shift;
+    uint64_t rem = mant & ((1ull << shift) - 1ull);
+    uint64_t half = 1ull << (shift - 1);
+    q += (rem > half || (rem == half && (q & 1ull))) ? 1ull : 0ull;
+    if (q >= 256ull) { q >>= 1; qexp += 1; }
+    if (q >= 128ull) {
+        int biased = qexp + 134;
+        if (biased >= 255) return (uint16_t)(sign | 0x7F80u);
+        return (uint16_t)(sign | (uint16_t)(biased << 7) | (uint16_t)(q & 127ull));
+    }
+    return (uint16_t)(sign | (uint16_t)q);
+}
+
+// silu(g) * u with an overflow-free logistic: for g << 0, exp(-g) -> inf and
+// g / inf -> -0, which is the limit.
+__device__ inline float silu_mul(float g, float u)
+{
+    return g / (1.0f + __expf(-g)) * u;
+}
+
+__device__ inline f32x4_t mfma16x16x32(const u32x4_t a, const u32x4_t b, f32x4_t c)
+{
+    return __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, a),
+                                                   __builtin_bit_cast(bf16x8_t, b), c, 0, 0, 0);
+}
+
+// Workspace routing block shared by the kernels (device pointers).
+struct RouteView {
+    float* logits;        // [Tm, E]
+    int32_t* topk_idx;    // [Tm, k]
+    float* topk_w;        // [Tm, k]
+    int32_t* counts;      // [E]
+    int32_t* offsets;     // [E + 1]
+    int32_t* pair_row;    // [Tm * k]
+    int32_t* row_token;   // [Tm * k]
+    int32_t* active;      // [E + 1]: active[0] = #local experts with tokens, then their ids
+    int32_t* tiles;       // [max_tiles * 2]: (expert, first row) per token tile; [.. ] count
+    int32_t* n_tiles;     // [1]
+};
+
+// Arguments of the decode expert kernels (moe_decode.hip).
+struct DecodeArgs {
+    const uint8_t* experts;   // arena: first local expert of this layer
+    uint64_t expert_bytes;    // stride between local experts
+    uint64_t gu_bytes;        // offset of DN inside an expert
+    const uint16_t* x;        // [T, d]
+    uint16_t* H;              // [rows, f]
+    float* O;                 // [rows, d]
+    const int32_t* active;    // [1 + E]
+    const int32_t* counts;    // [E]
+    const int32_t* offsets;   // [E + 1]
+    const int32_t* row_token; // [rows]
+    int d, f, e_begin;
+};
+
+// Arguments of the prefill grouped GEMM kernels (moe_prefill.hip).
+struct GemmArgs {
+    const uint8_t* experts;   // arena: first local expert of this layer
+    uint64_t expert_bytes;
+    uint64_t gu_bytes;
+    const uint16_t* x;        // [T, d]
+    uint16_t* H;              // [rows, f]
+    float* O;                 // [rows, d]
+    const int32_t* offsets;   // [E + 1]
+    const int32_t* row_token; // [rows]
+    const int32_t* tiles;     // [max_tiles][2] = (expert, first row)
+    const int32_t* n_tiles;   // [1]
+    int d, f, e_begin, max_tiles;
+};
+
+}  // namespace moe
+
+// Launchers (one per kernel family); each returns the launch status.
+extern "C" {
+hipError_t moe_launch_pack(const uint16_t* src, int K, int N, void* dst, int rt_mul, int rt_add,
+                           hipStream_t s);
+hipError_t moe_launch_router_partial(const uint16_t* x, const float* wr, int T, int d, int E,
+                                     int n_slices, double* partial, hipStream_t s);
+hipError_t moe_launch_route(const double* partial, const float* logits_in, const float* bias,
+                            int n_slices, int T, int E, int k, int e_begin, int n_local,
+                            int tile_rows, const moe::RouteView* rv, hipStream_t s);
+hipError_t moe_launch_decode(const moe::DecodeArgs* a, int n_slots, hipStream_t s);
+hipError_t moe_launch_prefill(const moe::GemmArgs* a, hipStream_t s);
+hipError_t moe_prefill_set_lds_limit();
+int moe_prefill_tile_rows();
+hipError_t moe_launch_combine(const float* O, const int32_t* pair_row, const float* topk_w, int T,
+                              int d, int k, uint16_t* y, uint16_t* x_residual, hipStream_t s);
+}

@@ -1,0 +1,137 @@
+// moe_decode.hip -- the expert FFN for small token counts (decode: at most 16
+// tokens per expert), streamed from HBM.
+//
+// Each wave owns one 16-feature tile of one active expert and walks the whole
+// reduction dimension.  The weight tile is the A operand of
+// v_mfma_f32_16x16x32_bf16 and the (at most 16) tokens of the expert are the
+// B operand, so the matrix cores do the dot products and the reduction over K;
+// the kernel is a pure 16-byte-per-lane stream of the packed weights (every
+// wave-wide load is 1 KiB contiguous).  Lanes whose token column is unused
+// feed zeros.
+//
+// gateup_kernel: G = x W1, U = x V1 for the 16 features, then
+//                H = bf16(silu(G) * U)          (paper Table tab:vars (e): w1, v1)
+// down_kernel:   O = H W2 for 16 output features, fp32
+//
+// Output fragment of the MFMA: lane l holds rows 4*(l/16)+r (r = 0..3) of
+// column l%16, i.e. four consecutive features of token slot l%16.
+#include "moe_common.h"
+
+namespace moe {
+
+constexpr int kUnroll = 8;
+
+__device__ inline u32x4_t ld16(const void* p)
+{
+    return __builtin_nontemporal_load(reinterpret_cast<const u32x4_t*>(p));
+}
+
+__device__ inline u32x4_t ld16_cached(const void* p)
+{
+    return *reinterpret_cast<const u32x4_t*>(p);
+}
+
+__global__ __launch_bounds__(64) void gateup_kernel(DecodeArgs a)
+{
+    const int n_ftiles = a.f / kTileRows;
+    const int slot = blockIdx.x / n_ftiles;
+    const int p = blockIdx.x % n_ftiles;
+    if (slot >= a.active[0]) return;
+    const int e = a.active[1 + slot];
+    const int m = a.counts[e];
+    const int row0 = a.offsets[e];
+    const int lane = threadIdx.x;
+    const int j = lane & 15;     // token slot (B column)
+    const int g = lane >> 4;     // K group of 8
+
+    const uint64_t KT = (uint64_t)a.d / kTileK;
+    const uint8_t* base = a.experts + (uint64_t)(e - a.e_begin) * a.expert_bytes;
+    const uint8_t* pg = base + tile_offset(2 * p, 0, KT) + lane * 16;
+    const uint8_t* pu = base + tile_offset(2 * p + 1, 0, KT) + lane * 16;
+    const bool has_tok = j < m;
+    const uint16_t* px = a.x + (has_tok ? (int64_t)a.row_token[row0 + j] * a.d : 0) + g * 8;
+
+    f32x4_t acc_g = {0.f, 0.f, 0.f, 0.f};
+    f32x4_t acc_u = {0.f, 0.f, 0.f, 0.f};
+    const u32x4_t zero = {0u, 0u, 0u, 0u};
+    for (uint64_t kt = 0; kt < KT; kt += kUnroll) {
+        u32x4_t wg[kUnroll], wu[kUnroll], xb[kUnroll];
+#pragma unroll
+        for (int u = 0; u < kUnroll; ++u) {
+            wg[u] = ld16(pg + (kt + u) * kTileBytes);
+            wu[u] = ld16(pu + (kt + u) * kTileBytes);
+        }
+#pragma unroll
+        for (int u = 0; u < kUnroll; ++u)
+            xb[u] = has_tok ? ld16_cached(px + (kt + u) * kTileK) : zero;
+#pragma unroll
+        for (int u = 0; u < kUnroll; ++u) {
+            acc_g = mfma16x16x32(wg[u], xb[u], acc_g);
+            acc_u = mfma16x16x32(wu[u], xb[u], acc_u);
+        }
+    }
+    if (has_tok) {
+        uint32_t h01 = (uint32_t)f32_to_bf16(silu_mul(acc_g[0], acc_u[0])) |
+                       ((uint32_t)f32_to_bf16(silu_mul(acc_g[1], acc_u[1])) << 16);
+        uint32_t h23 = (uint32_t)f32_to_bf16(silu_mul(acc_g[2], acc_u[2])) |
+                       ((uint32_t)f32_to_bf16(silu_mul(acc_g[3], acc_u[3])) << 16);
+        uint16_t* ph = a.H + (int64_t)(row0 + j) * a.f + p * kTileRows + g * 4;
+        *reinterpret_cast<uint2*>(ph) = make_uint2(h01, h23);
+    }
+}
+
+__global__ __launch_bounds__(64) void down_kernel(DecodeArgs a)
+{
+    const int n_otiles = a.d / kTileRows;
+    const int slot = blockIdx.x / n_otiles;
+    const int q = blockIdx.x % n_otiles;
+    if (slot >= a.active[0]) return;
+    const int e = a.active[1 + slot];
+    const int m = a.counts[e];
+    const int row0 = a.offsets[e];
+    const int lane = threadIdx.x;
+    const int j = lane & 15;
+    const int g = lane >> 4;
+
+    const uint64_t KT = (uint64_t)a.f / kTileK;
+    const uint8_t* base = a.experts + (uint64_t)(e - a.e_begin) * a.expert_bytes + a.gu_bytes;
+    const uint8_t* pw = base + tile_offset(q, 0, KT) + lane * 16;
+    const bool has_tok = j < m;
+    const uint16_t* ph = a.H + (has_tok ? (int64_t)(row0 + j) * a.f : 0) + g * 8;
+
+    f32x4_t acc = {0.f, 0.f, 0.f, 0.f};
+    const u32x4_t zero = {0u, 0u, 0u, 0u};
+    uint64_t kt = 0;
+    for (; kt + kUnroll <= KT; kt += kUnroll) {
+        u32x4_t w[kUnroll], hb[kUnroll];
+#pragma unroll
+        for (int u = 0; u < kUnroll; ++u) w[u] = ld16(pw + (kt + u) * kTileBytes);
+#pragma unroll
+        for (int u = 0; u < kUnroll; ++u)
+            hb[u] = has_tok ? ld16_cached(ph + (kt + u) * kTileK) : zero;
+#pragma unroll
+        for (int u = 0; u < kUnroll; ++u) acc = mfma16x16x32(w[u], hb[u], acc);
+    }
+    for (; kt < KT; ++kt) {
+        u32x4_t w = ld16(pw + kt * kTileBytes);
+        u32x4_t hb = has_tok ? ld16_cached(ph + kt * kTileK) : zero;
+        acc = mfma16x16x32(w, hb, acc);
+    }
+    if (has_tok) {
+        float* po = a.O + (int64_t)(row0 + j) * a.d + q * kTileRows + g * 4;
+        *reinterpret_cast<float4*>(po) = make_float4(acc[0], acc[1], acc[2], acc[3]);
+    }
+}
+
+}  // namespace moe
+
+extern "C" hipError_t moe_launch_decode(const moe::DecodeArgs* a, int n_slots, hipStream_t s)
+{
+    const int gu_blocks = n_slots * (a->f / moe::kTileRows);
+    const int dn_blocks = n_slots * (a->d / moe::kTileRows);
+    hipLaunchKernelGGL(moe::gateup_kernel, dim3(gu_blocks), dim3(64), 0, s, *a);
+    hipError_t err = hipGetLastError();
+    if (err != hipSuccess) return err;
+    hipLaunchKernelGGL(moe::down_kernel, dim3(dn_blocks), dim3(64), 0, s, *a);
+    return hipGetLastError();
+}

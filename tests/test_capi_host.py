@@ -1,0 +1,128 @@
+"""The C-ABI library on the host (no GPU needed): it loads, exports every
+symbol include/moe.h declares, and rejects bad arguments with the documented
+status codes before launching anything."""
+import ctypes
+import os
+import re
+
+import pytest
+
+import paper_2506_23635_amd as moe
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "moe.h")
+
+E_ARG, E_SHAPE, E_ALIGN, E_CAPACITY, E_STATE = -1, -2, -3, -4, -5
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    return sorted(set(re.findall(r"MOE_API\s+[\w\s\*]*?\b(moe_\w+)\s*\(", text)))
+
+
+def test_header_declares_the_boundary():
+    names = declared_functions()
+    for must in ("moe_init", "moe_route", "moe_forward", "moe_load_expert", "moe_load_router",
+                 "moe_weight_bytes", "moe_workspace_bytes", "moe_forward_stack", "moe_destroy",
+                 "moe_last_error"):
+        assert must in names
+    assert sorted(moe.EXPORTED) == names
+
+
+def test_library_exports_every_declared_symbol():
+    lib = moe.lib()
+    for name in declared_functions():
+        assert hasattr(lib, name), name
+
+
+def dbrx(**kw):
+    base = dict(d_model=6144, ffn_dim=10752, n_experts=16, top_k=4, n_layers=1, max_tokens=2048)
+    base.update(kw)
+    return moe.make_config(**base)
+
+
+def test_weight_bytes_formula():
+    cfg = dbrx()
+    expert = 3 * 6144 * 10752 * 2
+    router = 6144 * 16 * 4 + 256
+    assert moe.moe_weight_bytes(cfg) == 16 * expert + router
+    share = dbrx(expert_begin=4, n_local_experts=4, n_layers=32)
+    assert moe.moe_weight_bytes(share) == 32 * (4 * expert + router)
+    assert moe.moe_workspace_bytes(cfg) > 2048 * 4 * (10752 * 2 + 6144 * 4)
+
+
+@pytest.mark.parametrize("bad", [dict(d_model=100), dict(d_model=0), dict(ffn_dim=96),
+                                 dict(n_experts=0), dict(n_experts=65), dict(top_k=0),
+                                 dict(top_k=17), dict(expert_begin=13, n_local_experts=4),
+                                 dict(n_layers=0), dict(max_tokens=0), dict(flags=1)])
+def test_bad_configs_rejected(bad):
+    cfg = dbrx(**bad)
+    if bad.get("n_experts") == 0:
+        cfg.n_local_experts = 0
+    assert moe.moe_weight_bytes(cfg) == 0
+    assert moe.moe_workspace_bytes(cfg) == 0
+    out = ctypes.c_void_p()
+    rc = moe.lib().moe_init(ctypes.byref(cfg), 4096, 8192, ctypes.byref(out))
+    assert rc == E_SHAPE and out.value is None
+    assert moe.moe_last_error(None)
+
+
+def test_init_pointer_checks():
+    cfg = moe.make_config(256, 512, 8, 2, max_tokens=16)
+    out = ctypes.c_void_p()
+    assert moe.lib().moe_init(ctypes.byref(cfg), None, 4096, ctypes.byref(out)) == E_ARG
+    assert moe.lib().moe_init(ctypes.byref(cfg), 4096 + 16, 8192, ctypes.byref(out)) == E_ALIGN
+    assert moe.lib().moe_init(ctypes.byref(cfg), 4096, 8192, None) == E_ARG
+
+
+@pytest.fixture
+def fake_ctx():
+    # fake 256-aligned device addresses: nothing below ever dereferences them,
+    # because every call here fails validation before launching
+    cfg = moe.make_config(256, 512, 8, 2, expert_begin=2, n_local_experts=4, n_layers=2,
+                          max_tokens=16)
+    ctx = moe.moe_init(cfg, 1 << 20, 1 << 24)
+    yield ctx
+    moe.moe_destroy(ctx)
+
+
+def rc_of(fn, *args):
+    return getattr(moe.lib(), fn)(*args)
+
+
+def test_ctx_validation_before_any_launch(fake_ctx):
+    L = moe.lib()
+    r = moe.MoeRouting()
+    # layer out of range, router not loaded, capacity
+    assert L.moe_route(fake_ctx, 2, 4096, 1, None, ctypes.byref(r), None) == E_ARG
+    assert L.moe_route(fake_ctx, 0, 4096, 1, None, ctypes.byref(r), None) == E_STATE
+    assert "router" in moe.moe_last_error(fake_ctx)
+    assert L.moe_route(fake_ctx, 0, 4096, 17, None, ctypes.byref(r), None) == E_CAPACITY
+    assert L.moe_route(fake_ctx, 0, 4096, -1, None, ctypes.byref(r), None) == E_ARG
+    assert L.moe_route(fake_ctx, 0, 4096, 1, None, None, None) == E_ARG
+    # forward before loading
+    assert L.moe_forward(fake_ctx, 0, 4096, 1, None, 8192, None) == E_STATE
+    assert L.moe_forward(fake_ctx, 5, 4096, 1, None, 8192, None) == E_ARG
+    assert L.moe_forward(fake_ctx, 0, 4096, 99, None, 8192, None) == E_CAPACITY
+    assert L.moe_forward_stack(fake_ctx, 4096, 1, None) == E_STATE
+    # experts outside the local range [2, 6), null and misaligned pointers
+    assert L.moe_load_expert(fake_ctx, 0, 1, 4096, 4096, 4096, 1, None) == E_ARG
+    assert L.moe_load_expert(fake_ctx, 0, 6, 4096, 4096, 4096, 1, None) == E_ARG
+    assert L.moe_load_expert(fake_ctx, 2, 3, 4096, 4096, 4096, 1, None) == E_ARG
+    assert L.moe_load_expert(fake_ctx, 0, 3, None, 4096, 4096, 1, None) == E_ARG
+    assert L.moe_load_expert(fake_ctx, 0, 3, 4096 + 2, 4096, 4096, 1, None) == E_ALIGN
+    assert L.moe_load_router(fake_ctx, 0, None, None, 1, None) == E_ARG
+    assert L.moe_load_router(fake_ctx, -1, 4096, None, 1, None) == E_ARG
+
+
+def test_zero_tokens_route_is_empty_without_launch(fake_ctx):
+    # a zero-token call needs the router loaded but launches nothing; with
+    # the router not loaded it is a state error
+    r = moe.MoeRouting()
+    assert moe.lib().moe_route(fake_ctx, 0, None, 0, None, ctypes.byref(r), None) == E_STATE
+
+
+def test_status_strings():
+    L = moe.lib()
+    assert L.moe_status_string(0) == b"MOE_OK"
+    assert L.moe_status_string(-4) == b"MOE_E_CAPACITY"

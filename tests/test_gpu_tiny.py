@@ -1,0 +1,250 @@
+"""GPU parity on the small workload (16 tokens, d 256, 8 experts of ffn 512,
+top-2) and its variants, through the C-ABI, against the fp64 oracle."""
+import numpy as np
+import pytest
+
+import moe_inputs as mi
+import oracle
+from harness import (bf16_f64, check_layer_output, host_experts, load_workload_host,
+                     make_layer, rel_l2, to_np_u16, x_device)
+
+pytestmark = pytest.mark.gpu
+
+TINY = mi.WORKLOADS["tiny"]
+
+
+@pytest.fixture(scope="module")
+def torch_mod():
+    import torch
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    return torch
+
+
+def _oracle_full(wl, x, layer_idx=0, e_begin=0, n_local=0):
+    G, U, D = host_experts(wl, range(wl.E), layer_idx)
+    return oracle.layer(x, wl.router(layer_idx), wl.bias(layer_idx), G, U, D, wl.k,
+                        e_begin=e_begin, n_local=n_local)
+
+
+def test_device_generator_matches_host(torch_mod):
+    torch = torch_mod
+    for kind, n, sigma in ((mi.KIND_GATE, 100_003, 0.02), (mi.KIND_X, 4096, 1.0)):
+        st = mi.stream_id(kind, 3, 5)
+        t = torch.empty(n, dtype=torch.int16, device="cuda")
+        mi.gen_bf16_device(7, st, n, sigma, t.data_ptr(), torch.cuda.current_stream().cuda_stream)
+        torch.cuda.synchronize()
+        assert np.array_equal(to_np_u16(t), mi.gen_bf16(7, st, (n,), sigma))
+    f = torch.empty(5000, dtype=torch.float32, device="cuda")
+    mi.gen_f32_device(1, mi.stream_id(mi.KIND_ROUTER), 5000, 0.02, f.data_ptr(),
+                      torch.cuda.current_stream().cuda_stream)
+    torch.cuda.synchronize()
+    assert np.array_equal(f.cpu().numpy(), mi.gen_f32(1, mi.stream_id(mi.KIND_ROUTER), (5000,), 0.02))
+
+
+@pytest.fixture(scope="module")
+def tiny_layer(torch_mod):
+    layer = make_layer(TINY, max_tokens=512)
+    load_workload_host(layer, TINY)
+    yield layer
+    layer.close()
+
+
+def _check_routing(got, idx, w, E, e_begin=0, n_local=0):
+    assert np.array_equal(got["idx"], idx)
+    assert np.abs(got["w"].astype(np.float64) - w).max() <= 2e-6
+    counts, offsets, pair_row, row_token = oracle.permutation(idx, E, e_begin, n_local)
+    assert np.array_equal(got["counts"], counts)
+    assert np.array_equal(got["offsets"], offsets)
+    assert np.array_equal(got["pair_row"], pair_row)
+    assert np.array_equal(got["row_token"], row_token)
+
+
+def test_route_given_logits_bit_exact(torch_mod, tiny_layer):
+    torch = torch_mod
+    x_t, x = x_device(TINY)
+    lg = oracle.router_logits(x, TINY.router())
+    r = tiny_layer.route(0, x_t, logits_in=torch.from_numpy(lg).cuda())
+    got = tiny_layer.routing_tensors(r)
+    idx, w = oracle.route_from_logits(lg, TINY.k)
+    assert np.array_equal(got["logits"], lg)
+    _check_routing(got, idx, w, TINY.E)
+
+
+@pytest.mark.parametrize("case", ["ties", "signed_zero", "equal_rows", "one_token", "max_tokens"])
+def test_route_adversarial_logits(torch_mod, tiny_layer, case):
+    torch = torch_mod
+    E, k = TINY.E, TINY.k
+    rng = np.random.default_rng(len(case))
+    if case == "ties":
+        lg = rng.integers(-1, 2, size=(64, E)).astype(np.float32)
+    elif case == "signed_zero":
+        lg = np.where(rng.random((32, E)) < 0.5, -0.0, 0.0).astype(np.float32)
+        lg[:, E - 1] = -1.0
+    elif case == "equal_rows":
+        lg = np.tile(rng.standard_normal((1, E)).astype(np.float32), (40, 1))
+    elif case == "one_token":
+        lg = rng.standard_normal((1, E)).astype(np.float32)
+    else:
+        lg = rng.standard_normal((512, E)).astype(np.float32) * 3
+    T = lg.shape[0]
+    x_t = torch.zeros((T, TINY.d), dtype=torch.int16, device="cuda")
+    r = tiny_layer.route(0, x_t, logits_in=torch.from_numpy(lg).cuda())
+    got = tiny_layer.routing_tensors(r)
+    idx, w = oracle.route_from_logits(lg, k)
+    _check_routing(got, idx, w, E)
+
+
+def test_route_from_x_matches_oracle(torch_mod, tiny_layer):
+    x_t, x = x_device(TINY)
+    r = tiny_layer.route(0, x_t)
+    got = tiny_layer.routing_tensors(r)
+    lg = oracle.router_logits(x, TINY.router())
+    assert np.all(np.abs(got["logits"] - lg) <= 1e-5 * np.abs(lg).max())
+    assert np.mean(got["logits"] == lg) >= 0.99
+    idx, w = oracle.route_from_logits(lg, TINY.k)
+    _check_routing(got, idx, w, TINY.E)
+
+
+def _forward(torch, layer, x_t, T=None):
+    T = x_t.shape[0] if T is None else T
+    y = torch.empty((T, layer.cfg.d_model), dtype=torch.int16, device="cuda")
+    layer.forward(0, x_t, y, T=T)
+    torch.cuda.synchronize()
+    return to_np_u16(y)
+
+
+@pytest.mark.parametrize("T", [1, 5, 16])
+def test_forward_decode_path(torch_mod, tiny_layer, T):
+    torch = torch_mod
+    wl = TINY.with_(T=T)
+    x_t, x = x_device(wl)
+    y = _forward(torch, tiny_layer, x_t)
+    ref = _oracle_full(wl, x)
+    check_layer_output(y, ref["y64"])
+
+
+@pytest.mark.parametrize("T", [17, 100, 300, 512])
+def test_forward_gemm_path(torch_mod, tiny_layer, T):
+    torch = torch_mod
+    wl = TINY.with_(T=T)
+    x_t, x = x_device(wl)
+    y = _forward(torch, tiny_layer, x_t)
+    ref = _oracle_full(wl, x)
+    check_layer_output(y, ref["y64"])
+
+
+@pytest.mark.parametrize("T", [3, 200])
+def test_intermediate_h_within_fp32_error_bound(torch_mod, tiny_layer, T):
+    """H (the SiLU-gated activations) per grouped row vs the oracle's hb.
+
+    The GPU sums g = x.w1 and u = x.v1 in fp32, so beyond the final bf16
+    rounding its H may differ where a sum cancels.  Bound per element: one bf16
+    step of the reference plus the fp32 dot-product error bound
+    gamma_d * sum|x_i w_i| (gamma_d = d u / (1 - d u), u = 2^-24), carried
+    through h = silu(g) u to first order, plus a few fp32 ulps for the
+    logistic."""
+    import paper_2506_23635_amd as moe
+    torch = torch_mod
+    wl = TINY.with_(T=T)
+    x_t, x = x_device(wl)
+    _forward(torch, tiny_layer, x_t)
+    r = tiny_layer.route(0, x_t)   # same routing; H of the last forward stays
+    rt = tiny_layer.routing_tensors(r)
+    hptr, _ = moe.moe_intermediates(tiny_layer.ctx)
+    rows = int(rt["offsets"][-1])
+    H = torch.empty((rows, wl.f), dtype=torch.int16, device="cuda")
+    moe._copy_dev(H.data_ptr(), hptr, H.numel() * 2)
+    H = to_np_u16(H)
+    G, U, D = host_experts(wl, range(wl.E))
+    u32 = 2.0 ** -24
+    gamma = wl.d * u32 / (1 - wl.d * u32)
+    exact = []
+    for e in range(wl.E):
+        r0, r1 = rt["offsets"][e], rt["offsets"][e + 1]
+        if r1 == r0:
+            continue
+        xr = x[rt["row_token"][r0:r1]]
+        hb, _ = oracle.expert_glu(xr, G[e], U[e], D[e])
+        xf, w1, v1 = bf16_f64(xr), bf16_f64(G[e]), bf16_f64(U[e])
+        g, u = xf @ w1, xf @ v1
+        s1, s2 = np.abs(xf) @ np.abs(w1), np.abs(xf) @ np.abs(v1)
+        sig = 1.0 / (1.0 + np.exp(-g))
+        silu = g * sig
+        dsilu = sig * (1.0 + g * (1.0 - sig))
+        ref = bf16_f64(hb)
+        step = np.spacing(np.abs(ref).astype(np.float32)).astype(np.float64) * 65536.0
+        bound = step + gamma * (np.abs(dsilu * u) * s1 + np.abs(silu) * s2) + 8 * u32 * np.abs(silu * u)
+        err = np.abs(bf16_f64(H[r0:r1]) - ref)
+        assert np.all(err <= bound), float((err / bound).max())
+        exact.append(np.mean(_ordered(H[r0:r1]) == _ordered(hb)))
+    assert np.mean(exact) > 0.95
+
+
+def _ordered(bits):
+    """bf16 bit patterns as integers ordered like their values (+0 == -0)."""
+    b = np.asarray(bits, np.uint16).astype(np.int32)
+    mag = b & 0x7FFF
+    return np.where(b & 0x8000, -mag, mag)
+
+
+def test_expert_parallel_shares(torch_mod):
+    torch = torch_mod
+    wl = TINY
+    x_t, x = x_device(wl)
+    full = _oracle_full(wl, x)
+    total = np.zeros_like(full["y64"])
+    for s in range(4):
+        layer = make_layer(wl, max_tokens=wl.T, e_begin=2 * s, n_local=2)
+        load_workload_host(layer, wl)
+        y = _forward(torch, layer, x_t)
+        ref = _oracle_full(wl, x, e_begin=2 * s, n_local=2)
+        has = np.any((full["idx"] >= 2 * s) & (full["idx"] < 2 * s + 2), axis=1)
+        assert np.all(y[~has] & 0x7FFF == 0)
+        if has.any():
+            check_layer_output(y[has], ref["y64"][has])
+        total += bf16_f64(y)
+        layer.close()
+    assert rel_l2(total, full["y64"]) <= 2e-3
+
+
+def test_deterministic_bitwise(torch_mod, tiny_layer):
+    torch = torch_mod
+    for T in (16, 300):
+        x_t, _ = x_device(TINY.with_(T=T))
+        a = _forward(torch, tiny_layer, x_t)
+        b = _forward(torch, tiny_layer, x_t)
+        assert np.array_equal(a, b)
+
+
+def test_zero_tokens_and_capacity(torch_mod, tiny_layer):
+    import paper_2506_23635_amd as moe
+    torch = torch_mod
+    x_t = torch.zeros((1, TINY.d), dtype=torch.int16, device="cuda")
+    y = torch.full((1, TINY.d), 7, dtype=torch.int16, device="cuda")
+    tiny_layer.forward(0, x_t, y, T=0)
+    torch.cuda.synchronize()
+    assert int(y[0, 0]) == 7           # T == 0 enqueues nothing
+    with pytest.raises(moe.MoeError) as ei:
+        tiny_layer.forward(0, x_t, y, T=513)
+    assert ei.value.status == -4
+
+
+def test_stack_three_layers(torch_mod):
+    torch = torch_mod
+    wl = TINY.with_(T=4, n_layers=3)
+    layer = make_layer(wl, max_tokens=4)
+    for li in range(3):
+        load_workload_host(layer, wl, layer_idx=li)
+    x_t, x = x_device(wl)
+    layer.forward_stack(x_t)
+    torch.cuda.synchronize()
+    got = to_np_u16(x_t)
+    # oracle chain, teacher-forced per layer on the GPU's own layer input is
+    # not observable here, so compare the end-to-end chain
+    cur = x
+    for li in range(3):
+        ref = _oracle_full(wl, cur, layer_idx=li)
+        cur = oracle.residual_add(cur, ref["y"])
+    assert rel_l2(bf16_f64(got), bf16_f64(cur)) <= 2e-3
+    layer.close()
