@@ -1,0 +1,217 @@
+"""Benchmark of the DBRX-shaped MoE layer on one MI355X.
+
+Headline workload: one decode token through the whole 16-expert layer
+(d_model 6144, ffn 10752, top-4, bf16 weights ~N(0, 0.006)); one step = one
+moe_forward (router, selection, permutation, gate/up + SiLU, down, weighted
+combine) on inputs already resident in HBM.  The prefill layer (2048 tokens,
+N(0,1) weights, skewed routing) is timed in the same run and reported under
+"prefill".  The fp64 CPU oracle is timed on a bounded sample of the decode
+workload as a baseline.
+
+Prints one JSON line.  Usage: python bench.py [--gpus 1] [--steps K] [--warmup W]
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "DBRX-shape MoE layer: decode µs/layer + HBM GB/s; prefill tokens/s + MFMA %"
+HBM_PEAK_GBS = 8000.0          # MI355X HBM3E, GB/s
+MFMA_BF16_PEAK_TFLOPS = 2500.0  # MI355X dense bf16 matrix, TFLOP/s
+
+
+def log(msg):
+    print(msg, file=sys.stderr, flush=True)
+
+
+def setup_layer(wl, max_tokens):
+    import torch
+    import moe_inputs as mi
+    import paper_2506_23635_amd as moe
+    cfg = moe.make_config(wl.d, wl.f, wl.E, wl.k, max_tokens=max_tokens)
+    layer = moe.MoeLayer(cfg)
+    s = layer.stream
+    d, f, E = wl.d, wl.f, wl.E
+    wr = torch.empty(d * E, dtype=torch.float32, device="cuda")
+    mi.gen_f32_device(wl.seed, mi.stream_id(mi.KIND_ROUTER), d * E, wl.sigma_r, wr.data_ptr(), s)
+    b = None
+    if wl.sigma_b:
+        b = torch.empty(E, dtype=torch.float32, device="cuda")
+        mi.gen_f32_device(wl.seed, mi.stream_id(mi.KIND_BIAS), E, wl.sigma_b, b.data_ptr(), s)
+    layer.load_router(0, wr, b)
+    stg = torch.empty(3 * d * f, dtype=torch.int16, device="cuda")
+    g, u, dn = stg[: d * f], stg[d * f: 2 * d * f], stg[2 * d * f:]
+    for e in range(E):
+        mi.gen_bf16_device(wl.seed, mi.stream_id(mi.KIND_GATE, 0, e), d * f, wl.sigma_w, g.data_ptr(), s)
+        mi.gen_bf16_device(wl.seed, mi.stream_id(mi.KIND_UP, 0, e), d * f, wl.sigma_w, u.data_ptr(), s)
+        mi.gen_bf16_device(wl.seed, mi.stream_id(mi.KIND_DOWN, 0, e), d * f, wl.sigma_w, dn.data_ptr(), s)
+        layer.load_expert(0, e, g, u, dn)
+    x = torch.empty(wl.T * d, dtype=torch.int16, device="cuda")
+    mi.gen_bf16_device(wl.seed, mi.stream_id(mi.KIND_X), wl.T * d, wl.sigma_x, x.data_ptr(), s)
+    torch.cuda.synchronize()
+    del stg
+    return layer, x.view(wl.T, d)
+
+
+def time_layer(layer, x, steps, warmup):
+    """Runs warmup + timed steps; returns (ms_per_step, per-kernel ms/launch, counts)."""
+    import torch
+    import paper_2506_23635_amd as moe
+    T = x.shape[0]
+    y = torch.empty((T, layer.cfg.d_model), dtype=torch.int16, device="cuda")
+    for _ in range(warmup):
+        layer.forward(0, x, y)
+    torch.cuda.synchronize()
+    moe.moe_profile_enable(layer.ctx, 8 * steps + 8)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(steps):
+        layer.forward(0, x, y)
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    prof, dropped = moe.moe_profile_read(layer.ctx)
+    moe.moe_profile_enable(layer.ctx, 0)
+    r = layer.route(0, x)
+    rt = layer.routing_tensors(r)
+    per_kernel = {k: {"ms_per_launch": v[0] / v[1], "launches": v[1]}
+                  for k, v in prof.items() if v[1]}
+    return (t1 - t0) * 1e3 / steps, per_kernel, rt, dropped
+
+
+def cpu_baseline(wl, budget_s=10.0):
+    """The fp64 oracle on the decode token of the workload, repeated for about
+    budget_s seconds of host time (weights generated before the clock)."""
+    import numpy as np
+    import moe_inputs as mi
+    import oracle
+    x = wl.x()
+    lg = oracle.router_logits(x, wl.router())
+    idx, _ = oracle.route_from_logits(lg, wl.k)
+    used = sorted(set(idx.reshape(-1).tolist()))
+    G = [None] * wl.E
+    U = [None] * wl.E
+    D = [None] * wl.E
+    for e in used:
+        G[e], U[e], D[e] = wl.gate(e), wl.up(e), wl.down(e)
+    wr = wl.router()
+    reps = 0
+    t0 = time.perf_counter()
+    while True:
+        oracle.layer(x, wr, wl.bias(), G, U, D, wl.k)
+        reps += 1
+        el = time.perf_counter() - t0
+        if el >= budget_s or reps >= 50:
+            break
+    threads = int(os.environ.get("OMP_NUM_THREADS", "0") or 0) or os.cpu_count()
+    assert np.isfinite(el)
+    return {"value": reps * wl.T / el, "unit": "tokens/s", "cores": threads, "kind": "oracle",
+            "sample": f"decode token (T={wl.T}) through the full 16-expert layer, {reps} "
+                      f"repetitions, {el:.1f} s of host time, fp64 oracle with OpenMP"}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=100)
+    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--prefill-steps", type=int, default=20)
+    ap.add_argument("--no-prefill", action="store_true")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU only: this build has no multi-GPU path "
+              f"(--gpus {args.gpus} requested)", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    import moe_inputs as mi
+    if not torch.cuda.is_available():
+        print("bench.py needs a GPU", file=sys.stderr)
+        sys.exit(1)
+    import paper_2506_23635_amd as moe
+    moe.lib()   # raises if the HIP library is not built
+
+    wl = mi.WORKLOADS["decode"]
+    log("setup decode layer (16 experts, 6.3 GB) ...")
+    layer, x = setup_layer(wl, max_tokens=wl.T)
+    log("timing decode ...")
+    ms, kern, rt, dropped = time_layer(layer, x, args.steps, args.warmup)
+    touched = int((rt["counts"] > 0).sum())
+    expert_bytes = 3 * wl.d * wl.f * 2
+    gu_unit = 2 * wl.d * wl.f * 2                     # one touched expert's gate+up
+    layer_bytes = touched * expert_bytes + wl.d * wl.E * 4 + 2 * wl.T * wl.d * 2
+    us = ms * 1e3
+    hbm_gbs = layer_bytes / (ms * 1e-3) / 1e9
+    gu = kern["decode_gateup"]
+    gu_bytes = touched * gu_unit + wl.T * wl.d * 2
+    gu_gbs = gu_bytes / (gu["ms_per_launch"] * 1e-3) / 1e9
+    layer.close()
+    del layer, x
+    torch.cuda.empty_cache()
+
+    prefill = None
+    if not args.no_prefill:
+        pw = mi.WORKLOADS["prefill"]
+        log("setup prefill layer ...")
+        player, px = setup_layer(pw, max_tokens=pw.T)
+        log("timing prefill ...")
+        pms, pkern, prt, _ = time_layer(player, px, args.prefill_steps, 3)
+        rows = int(prt["offsets"][-1])
+        flops = 2.0 * rows * 3 * pw.d * pw.f
+        tflops = flops / (pms * 1e-3) / 1e12
+        g1 = pkern["gemm_gateup"]
+        g1_flops = 2.0 * rows * 2 * pw.d * pw.f
+        prefill = {
+            "workload": "dbrx_moe_layer_prefill", "T": pw.T, "tokens_per_s": pw.T / (pms * 1e-3),
+            "ms_per_layer": pms, "tflops": tflops, "mfma_frac": tflops / MFMA_BF16_PEAK_TFLOPS,
+            "expert_counts": prt["counts"].tolist(),
+            "kernels_ms": {k: v["ms_per_launch"] for k, v in pkern.items()},
+            "gemm_gateup_tflops": g1_flops / (g1["ms_per_launch"] * 1e-3) / 1e12,
+        }
+        player.close()
+        del player, px
+        torch.cuda.empty_cache()
+
+    cpu = None
+    if not args.no_cpu_baseline:
+        log("timing the CPU oracle ...")
+        cpu = cpu_baseline(wl)
+
+    out = {
+        "metric": METRIC,
+        "value": wl.T / (ms * 1e-3),
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {"workload": "dbrx_moe_layer_decode", "T": wl.T, "d_model": wl.d,
+                   "ffn_dim": wl.f, "n_experts": wl.E, "top_k": wl.k, "parallelism": "none"},
+        "us_per_layer": us,
+        "hbm_gbs": hbm_gbs,
+        "hbm_frac": hbm_gbs / HBM_PEAK_GBS,
+        "touched_experts": touched,
+        "roofline": {"bound": "hbm", "kernel": "decode_gateup", "achieved": gu_gbs,
+                     "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": gu_gbs / HBM_PEAK_GBS,
+                     "traffic": None},
+        "kernels_us": {k: v["ms_per_launch"] * 1e3 for k, v in kern.items()},
+        "profile_dropped": dropped,
+        "cpu_baseline": cpu,
+        "prefill": prefill,
+    }
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

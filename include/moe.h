@@ -170,7 +170,31 @@ MOE_API moe_status moe_forward_stack(moe_ctx *ctx, uint16_t *x_inout, int32_t T,
 MOE_API moe_status moe_intermediates(const moe_ctx *ctx, const uint16_t **h,
                              const float **o);
 
-/* Frees the host-side context (never the caller's device buffers). */
+/* Per-kernel timing for measurement harnesses.  moe_profile_enable(ctx, n)
+ * with n > 0 creates 2n HIP events and from then on brackets each kernel
+ * launch of the context with an event pair on the launch stream (at most n
+ * launches between reads; later ones run untimed and are counted as
+ * dropped); n == 0 turns timing off and frees the events.
+ * moe_profile_read waits for the recorded launches, writes per kind the total
+ * milliseconds and the launch count (arrays of MOE_K_COUNT), the number of
+ * dropped launches (may be NULL), and starts a new recording. */
+typedef enum {
+    MOE_K_ROUTER = 0,        /* router logits, fp64 partial sums */
+    MOE_K_ROUTE = 1,         /* selection, weights, permutation */
+    MOE_K_DECODE_GATEUP = 2, /* small-T gate/up + SiLU */
+    MOE_K_DECODE_DOWN = 3,   /* small-T down projection */
+    MOE_K_GEMM_GATEUP = 4,   /* grouped GEMM gate/up + SiLU */
+    MOE_K_GEMM_DOWN = 5,     /* grouped GEMM down projection */
+    MOE_K_COMBINE = 6,       /* weighted combine (and residual) */
+    MOE_K_PACK = 7,          /* expert prestacking */
+    MOE_K_COUNT = 8
+} moe_kernel_kind;
+MOE_API moe_status moe_profile_enable(moe_ctx *ctx, int32_t max_launches);
+MOE_API moe_status moe_profile_read(moe_ctx *ctx, double *total_ms,
+                                    int64_t *launches, int64_t *dropped);
+
+/* Frees the host-side context and its profiling events (never the caller's
+ * device buffers). */
 MOE_API void moe_destroy(moe_ctx *ctx);
 
 /* Message of the last failing call on ctx ("" if none); with ctx == NULL,

@@ -21,7 +21,11 @@ STATUS_NAMES = {0: "MOE_OK", -1: "MOE_E_ARG", -2: "MOE_E_SHAPE", -3: "MOE_E_ALIG
 
 EXPORTED = ["moe_weight_bytes", "moe_workspace_bytes", "moe_init", "moe_load_expert",
             "moe_load_router", "moe_route", "moe_forward", "moe_forward_stack",
-            "moe_intermediates", "moe_destroy", "moe_last_error", "moe_status_string"]
+            "moe_intermediates", "moe_profile_enable", "moe_profile_read", "moe_destroy",
+            "moe_last_error", "moe_status_string"]
+
+KERNEL_KINDS = ["router", "route", "decode_gateup", "decode_down", "gemm_gateup", "gemm_down",
+                "combine", "pack"]
 
 
 class MoeConfig(ctypes.Structure):
@@ -72,6 +76,8 @@ def lib():
         L.moe_forward.argtypes = [P, I, P, I, ctypes.POINTER(MoeRouting), P, P]
         L.moe_forward_stack.argtypes = [P, P, I, P]
         L.moe_intermediates.argtypes = [P, ctypes.POINTER(P), ctypes.POINTER(P)]
+        L.moe_profile_enable.argtypes = [P, I]
+        L.moe_profile_read.argtypes = [P, P, P, P]
         L.moe_destroy.argtypes = [P]
         L.moe_destroy.restype = None
         L.moe_last_error.argtypes = [P]
@@ -79,7 +85,8 @@ def lib():
         L.moe_status_string.argtypes = [ctypes.c_int]
         L.moe_status_string.restype = ctypes.c_char_p
         for fn in ("moe_init", "moe_load_expert", "moe_load_router", "moe_route", "moe_forward",
-                   "moe_forward_stack", "moe_intermediates"):
+                   "moe_forward_stack", "moe_intermediates", "moe_profile_enable",
+                   "moe_profile_read"):
             getattr(L, fn).restype = ctypes.c_int
         _lib = L
     return _lib
@@ -140,6 +147,20 @@ def moe_intermediates(ctx):
     o = ctypes.c_void_p()
     _check(ctx, lib().moe_intermediates(ctx, ctypes.byref(h), ctypes.byref(o)))
     return h.value, o.value
+
+
+def moe_profile_enable(ctx, max_launches: int):
+    _check(ctx, lib().moe_profile_enable(ctx, max_launches))
+
+
+def moe_profile_read(ctx):
+    """{kind: (total_ms, launches)} since the last read, and the dropped count."""
+    n = len(KERNEL_KINDS)
+    ms = (ctypes.c_double * n)()
+    cnt = (ctypes.c_int64 * n)()
+    dropped = ctypes.c_int64()
+    _check(ctx, lib().moe_profile_read(ctx, ms, cnt, ctypes.byref(dropped)))
+    return {k: (ms[i], cnt[i]) for i, k in enumerate(KERNEL_KINDS)}, dropped.value
 
 
 def moe_destroy(ctx):

@@ -20,7 +20,6 @@
 namespace {
 
 constexpr int kDecodeMaxTokens = 16;   // token columns of one MFMA B operand
-constexpr int kMaxSlices = 64;
 constexpr size_t kAlign = 256;
 
 size_t align_up(size_t v, size_t a) { return (v + a - 1) / a * a; }
@@ -30,7 +29,7 @@ struct Layout {
     size_t router_bytes, bias_off, gu_bytes, dn_bytes, expert_bytes, experts_off, layer_bytes;
     size_t arena_bytes;
     // workspace
-    size_t partial_off, logits_off, idx_off, w_off, counts_off, offsets_off, pair_row_off,
+    size_t dpart_off, counter_off, logits_off, idx_off, w_off, counts_off, offsets_off, pair_row_off,
         row_token_off, active_off, tiles_off, n_tiles_off, h_off, o_off, ws_bytes;
     int rows_max, max_tiles;
 };
@@ -71,8 +70,8 @@ Layout make_layout(const moe_config* c)
     L.max_tiles = (int)((L.rows_max + tile_rows - 1) / tile_rows + nl);
     size_t off = 0;
     auto take = [&](size_t bytes) { size_t o = off; off = align_up(off + bytes, kAlign); return o; };
-    const size_t partial_elems = std::max((size_t)65536, Tm * E);
-    L.partial_off = take(partial_elems * 8);
+    L.dpart_off = take((size_t)moe_route_decode_wgs(c->d_model) * 16 * 16 * 8);
+    L.counter_off = take(4);
     L.logits_off = take(Tm * E * 4);
     L.idx_off = take(Tm * k * 4);
     L.w_off = take(Tm * k * 4);
@@ -103,6 +102,12 @@ struct moe_ctx {
     std::vector<uint8_t> expert_loaded;   // [n_layers * n_local]
     moe::RouteView rv;
     bool gemm_lds_set;      // dynamic-LDS limit raised for the GEMM kernels
+    bool counter_ready;     // decode-route ticket counter zeroed on this workspace
+    // per-kernel timing (moe_profile_*): an event pair around each launch
+    bool prof_on;
+    std::vector<hipEvent_t> prof_events;   // 2 per launch slot
+    std::vector<int> prof_kinds;           // kind of each recorded launch
+    int64_t prof_dropped;
     // last routing
     bool route_valid;
     int route_layer, route_T;
@@ -126,15 +131,27 @@ moe_status hip_fail(moe_ctx* ctx, hipError_t e, const char* what)
     return fail(ctx, MOE_E_HIP, std::string(what) + ": " + hipGetErrorString(e));
 }
 
-uint8_t* layer_base(moe_ctx* c, int layer) { return c->arena + (size_t)layer * c->L.layer_bytes; }
-
-int n_slices_for(int T, int E)
+// Runs one launch; with profiling on, brackets it with a pair of events on
+// the launch stream.
+template <class F>
+hipError_t timed(moe_ctx* c, int kind, hipStream_t s, F&& launch)
 {
-    long long s = 65536LL / ((long long)T * E);
-    if (s < 1) s = 1;
-    if (s > kMaxSlices) s = kMaxSlices;
-    return (int)s;
+    if (!c->prof_on) return launch();
+    const size_t slot = c->prof_kinds.size();
+    if (2 * slot + 1 >= c->prof_events.size()) {
+        ++c->prof_dropped;
+        return launch();
+    }
+    hipError_t e = hipEventRecord(c->prof_events[2 * slot], s);
+    if (e != hipSuccess) return e;
+    e = launch();
+    if (e != hipSuccess) return e;
+    e = hipEventRecord(c->prof_events[2 * slot + 1], s);
+    if (e == hipSuccess) c->prof_kinds.push_back(kind);
+    return e;
 }
+
+uint8_t* layer_base(moe_ctx* c, int layer) { return c->arena + (size_t)layer * c->L.layer_bytes; }
 
 moe_status check_layer(moe_ctx* ctx, int layer)
 {
@@ -151,20 +168,45 @@ moe_status do_route(moe_ctx* ctx, int layer, const uint16_t* x, int T, const flo
 {
     const moe_config& c = ctx->cfg;
     uint8_t* lb = layer_base(ctx, layer);
-    const float* wr = reinterpret_cast<const float*>(lb);
+    const float* wrT = reinterpret_cast<const float*>(lb);
     const float* bias = ctx->has_bias[layer] ? reinterpret_cast<const float*>(lb + ctx->L.bias_off)
                                              : nullptr;
-    double* partial = reinterpret_cast<double*>(ctx->ws + ctx->L.partial_off);
-    int n_slices = n_slices_for(T, c.n_experts);
+    const int tile_rows = moe_prefill_tile_rows();
     hipError_t e;
-    if (!logits_in) {
-        e = moe_launch_router_partial(x, wr, T, c.d_model, c.n_experts, n_slices, partial, s);
-        if (e != hipSuccess) return hip_fail(ctx, e, "router kernel launch");
+    if (!logits_in && moe_route_decode_ok(T, c.n_experts, c.top_k)) {
+        unsigned int* counter = reinterpret_cast<unsigned int*>(ctx->ws + ctx->L.counter_off);
+        if (!ctx->counter_ready) {
+            e = moe_launch_zero_counter(counter, s);
+            if (e != hipSuccess) return hip_fail(ctx, e, "counter init launch");
+            ctx->counter_ready = true;
+        }
+        double* dpart = reinterpret_cast<double*>(ctx->ws + ctx->L.dpart_off);
+        e = timed(ctx, MOE_K_ROUTE, s, [&] {
+            return moe_launch_route_decode(x, wrT, bias, dpart, counter, T, c.d_model, c.n_experts,
+                                           c.top_k, c.expert_begin, c.n_local_experts, tile_rows,
+                                           &ctx->rv, s);
+        });
+        if (e != hipSuccess) return hip_fail(ctx, e, "route kernel launch");
+    } else if (!logits_in && T <= moe_route_small_max_tokens()) {
+        e = timed(ctx, MOE_K_ROUTE, s, [&] {
+            return moe_launch_route_small(x, wrT, bias, T, c.d_model, c.n_experts, c.top_k,
+                                          c.expert_begin, c.n_local_experts, tile_rows, &ctx->rv, s);
+        });
+        if (e != hipSuccess) return hip_fail(ctx, e, "route kernel launch");
+    } else {
+        if (!logits_in) {
+            e = timed(ctx, MOE_K_ROUTER, s, [&] {
+                return moe_launch_router_logits(x, wrT, bias, T, c.d_model, c.n_experts,
+                                                ctx->rv.logits, s);
+            });
+            if (e != hipSuccess) return hip_fail(ctx, e, "router kernel launch");
+        }
+        e = timed(ctx, MOE_K_ROUTE, s, [&] {
+            return moe_launch_route(logits_in, T, c.n_experts, c.top_k, c.expert_begin,
+                                    c.n_local_experts, tile_rows, &ctx->rv, s);
+        });
+        if (e != hipSuccess) return hip_fail(ctx, e, "route kernel launch");
     }
-    e = moe_launch_route(logits_in ? nullptr : partial, logits_in, bias, n_slices, T, c.n_experts,
-                         c.top_k, c.expert_begin, c.n_local_experts, moe_prefill_tile_rows(),
-                         &ctx->rv, s);
-    if (e != hipSuccess) return hip_fail(ctx, e, "route kernel launch");
     ctx->route_valid = true;
     ctx->route_layer = layer;
     ctx->route_T = T;
@@ -208,8 +250,10 @@ moe_status run_experts(moe_ctx* ctx, int layer, const uint16_t* x, int T, hipStr
         a.f = c.ffn_dim;
         a.e_begin = c.expert_begin;
         int slots = std::min(c.n_local_experts, T * c.top_k);
-        e = moe_launch_decode(&a, slots, s);
-        if (e != hipSuccess) return hip_fail(ctx, e, "decode expert kernels launch");
+        e = timed(ctx, MOE_K_DECODE_GATEUP, s, [&] { return moe_launch_decode_gateup(&a, slots, s); });
+        if (e != hipSuccess) return hip_fail(ctx, e, "decode gate/up kernel launch");
+        e = timed(ctx, MOE_K_DECODE_DOWN, s, [&] { return moe_launch_decode_down(&a, slots, s); });
+        if (e != hipSuccess) return hip_fail(ctx, e, "decode down kernel launch");
     } else {
         moe::GemmArgs a;
         a.experts = experts;
@@ -233,8 +277,10 @@ moe_status run_experts(moe_ctx* ctx, int layer, const uint16_t* x, int T, hipStr
         const int tile_rows = moe_prefill_tile_rows();
         const int kl = std::min(c.top_k, c.n_local_experts);
         a.max_tiles = (T * kl + tile_rows - 1) / tile_rows + c.n_local_experts;
-        e = moe_launch_prefill(&a, s);
-        if (e != hipSuccess) return hip_fail(ctx, e, "prefill expert kernels launch");
+        e = timed(ctx, MOE_K_GEMM_GATEUP, s, [&] { return moe_launch_gemm_gateup(&a, s); });
+        if (e != hipSuccess) return hip_fail(ctx, e, "grouped GEMM gate/up kernel launch");
+        e = timed(ctx, MOE_K_GEMM_DOWN, s, [&] { return moe_launch_gemm_down(&a, s); });
+        if (e != hipSuccess) return hip_fail(ctx, e, "grouped GEMM down kernel launch");
     }
     return MOE_OK;
 }
@@ -300,6 +346,9 @@ moe_status moe_init(const moe_config* cfg, void* weight_arena, void* workspace, 
     c->rv.n_tiles = reinterpret_cast<int32_t*>(w + c->L.n_tiles_off);
     c->route_valid = false;
     c->gemm_lds_set = false;
+    c->counter_ready = false;
+    c->prof_on = false;
+    c->prof_dropped = 0;
     *out = c;
     return MOE_OK;
 }
@@ -322,9 +371,12 @@ moe_status moe_load_expert(moe_ctx* ctx, int32_t layer, int32_t expert, const ui
         if (misaligned(gate) || misaligned(up) || misaligned(down))
             return fail(ctx, MOE_E_ALIGN, "device weight pointers must be 16-byte aligned");
         hipError_t e;
-        if ((e = moe_launch_pack(gate, d, f, dst, 2, 0, s)) != hipSuccess ||
-            (e = moe_launch_pack(up, d, f, dst, 2, 1, s)) != hipSuccess ||
-            (e = moe_launch_pack(down, f, d, dst + ctx->L.gu_bytes, 1, 0, s)) != hipSuccess)
+        auto pk = [&](const uint16_t* src, int K, int N, uint8_t* to, int mul, int add) {
+            return timed(ctx, MOE_K_PACK, s, [&] { return moe_launch_pack(src, K, N, to, mul, add, s); });
+        };
+        if ((e = pk(gate, d, f, dst, 2, 0)) != hipSuccess ||
+            (e = pk(up, d, f, dst, 2, 1)) != hipSuccess ||
+            (e = pk(down, f, d, dst + ctx->L.gu_bytes, 1, 0)) != hipSuccess)
             return hip_fail(ctx, e, "pack kernel launch");
     } else {
         std::vector<uint8_t> tmp;
@@ -353,13 +405,30 @@ moe_status moe_load_router(moe_ctx* ctx, int32_t layer, const float* wr, const f
     if (!wr) return fail(ctx, MOE_E_ARG, "router weight is NULL");
     uint8_t* lb = layer_base(ctx, layer);
     hipStream_t s = static_cast<hipStream_t>(stream);
-    const size_t wbytes = (size_t)c.d_model * c.n_experts * 4;
-    const hipMemcpyKind kind = src_on_device ? hipMemcpyDeviceToDevice : hipMemcpyHostToDevice;
-    hipError_t e = hipMemcpyAsync(lb, wr, wbytes, kind, s);
-    if (e == hipSuccess && bias)
-        e = hipMemcpyAsync(lb + ctx->L.bias_off, bias, (size_t)c.n_experts * 4, kind, s);
-    if (e == hipSuccess && !src_on_device) e = hipStreamSynchronize(s);
-    if (e != hipSuccess) return hip_fail(ctx, e, "router copy");
+    const int d = c.d_model, E = c.n_experts;
+    float* wrT = reinterpret_cast<float*>(lb);
+    hipError_t e;
+    if (src_on_device) {
+        if (misaligned(wr) || (bias && misaligned(bias)))
+            return fail(ctx, MOE_E_ALIGN, "device router pointers must be 16-byte aligned");
+        e = timed(ctx, MOE_K_PACK, s, [&] { return moe_launch_transpose_router(wr, d, E, wrT, s); });
+        if (e == hipSuccess && bias)
+            e = hipMemcpyAsync(lb + ctx->L.bias_off, bias, (size_t)E * 4, hipMemcpyDeviceToDevice, s);
+    } else {
+        std::vector<float> tmp;
+        try {
+            tmp.resize((size_t)d * E);
+        } catch (...) {
+            return fail(ctx, MOE_E_ARG, "out of host memory for the router transpose");
+        }
+        for (int i = 0; i < d; ++i)
+            for (int ee = 0; ee < E; ++ee) tmp[(size_t)ee * d + i] = wr[(size_t)i * E + ee];
+        e = hipMemcpyAsync(wrT, tmp.data(), tmp.size() * 4, hipMemcpyHostToDevice, s);
+        if (e == hipSuccess && bias)
+            e = hipMemcpyAsync(lb + ctx->L.bias_off, bias, (size_t)E * 4, hipMemcpyHostToDevice, s);
+        if (e == hipSuccess) e = hipStreamSynchronize(s);
+    }
+    if (e != hipSuccess) return hip_fail(ctx, e, "router load");
     ctx->router_loaded[layer] = 1;
     ctx->has_bias[layer] = bias ? 1 : 0;
     return MOE_OK;
@@ -413,9 +482,11 @@ moe_status moe_forward(moe_ctx* ctx, int32_t layer, const uint16_t* x, int32_t T
     }
     st = run_experts(ctx, layer, x, T, s);
     if (st != MOE_OK) return st;
-    hipError_t e = moe_launch_combine(reinterpret_cast<const float*>(ctx->ws + ctx->L.o_off),
-                                      ctx->rv.pair_row, ctx->rv.topk_w, T, ctx->cfg.d_model,
-                                      ctx->cfg.top_k, y, nullptr, s);
+    hipError_t e = timed(ctx, MOE_K_COMBINE, s, [&] {
+        return moe_launch_combine(reinterpret_cast<const float*>(ctx->ws + ctx->L.o_off),
+                                  ctx->rv.pair_row, ctx->rv.topk_w, T, ctx->cfg.d_model,
+                                  ctx->cfg.top_k, y, nullptr, s);
+    });
     if (e != hipSuccess) return hip_fail(ctx, e, "combine kernel launch");
     return MOE_OK;
 }
@@ -438,9 +509,11 @@ moe_status moe_forward_stack(moe_ctx* ctx, uint16_t* x_inout, int32_t T, moe_str
         if (st != MOE_OK) return st;
         st = run_experts(ctx, l, x_inout, T, s);
         if (st != MOE_OK) return st;
-        hipError_t e = moe_launch_combine(reinterpret_cast<const float*>(ctx->ws + ctx->L.o_off),
-                                          ctx->rv.pair_row, ctx->rv.topk_w, T, ctx->cfg.d_model,
-                                          ctx->cfg.top_k, nullptr, x_inout, s);
+        hipError_t e = timed(ctx, MOE_K_COMBINE, s, [&] {
+            return moe_launch_combine(reinterpret_cast<const float*>(ctx->ws + ctx->L.o_off),
+                                      ctx->rv.pair_row, ctx->rv.topk_w, T, ctx->cfg.d_model,
+                                      ctx->cfg.top_k, nullptr, x_inout, s);
+        });
         if (e != hipSuccess) return hip_fail(ctx, e, "combine kernel launch");
     }
     return MOE_OK;
@@ -454,7 +527,56 @@ moe_status moe_intermediates(const moe_ctx* ctx, const uint16_t** h, const float
     return MOE_OK;
 }
 
-void moe_destroy(moe_ctx* ctx) { delete ctx; }
+moe_status moe_profile_enable(moe_ctx* ctx, int32_t max_launches)
+{
+    if (!ctx) return MOE_E_ARG;
+    if (max_launches < 0) return fail(ctx, MOE_E_ARG, "max_launches is negative");
+    for (hipEvent_t ev : ctx->prof_events) (void)hipEventDestroy(ev);
+    ctx->prof_events.clear();
+    ctx->prof_kinds.clear();
+    ctx->prof_dropped = 0;
+    ctx->prof_on = false;
+    if (max_launches == 0) return MOE_OK;
+    ctx->prof_events.resize(2 * (size_t)max_launches);
+    for (auto& ev : ctx->prof_events) {
+        hipError_t e = hipEventCreate(&ev);
+        if (e != hipSuccess) {
+            ev = nullptr;
+            return hip_fail(ctx, e, "event creation");
+        }
+    }
+    ctx->prof_kinds.reserve(max_launches);
+    ctx->prof_on = true;
+    return MOE_OK;
+}
+
+moe_status moe_profile_read(moe_ctx* ctx, double* total_ms, int64_t* launches, int64_t* dropped)
+{
+    if (!ctx) return MOE_E_ARG;
+    if (!total_ms || !launches) return fail(ctx, MOE_E_ARG, "output array is NULL");
+    for (int k = 0; k < MOE_K_COUNT; ++k) { total_ms[k] = 0.0; launches[k] = 0; }
+    for (size_t i = 0; i < ctx->prof_kinds.size(); ++i) {
+        hipError_t e = hipEventSynchronize(ctx->prof_events[2 * i + 1]);
+        float ms = 0.f;
+        if (e == hipSuccess)
+            e = hipEventElapsedTime(&ms, ctx->prof_events[2 * i], ctx->prof_events[2 * i + 1]);
+        if (e != hipSuccess) return hip_fail(ctx, e, "event timing");
+        total_ms[ctx->prof_kinds[i]] += ms;
+        launches[ctx->prof_kinds[i]] += 1;
+    }
+    if (dropped) *dropped = ctx->prof_dropped;
+    ctx->prof_kinds.clear();
+    ctx->prof_dropped = 0;
+    return MOE_OK;
+}
+
+void moe_destroy(moe_ctx* ctx)
+{
+    if (!ctx) return;
+    for (hipEvent_t ev : ctx->prof_events)
+        if (ev) (void)hipEventDestroy(ev);
+    delete ctx;
+}
 
 const char* moe_last_error(const moe_ctx* ctx)
 {

@@ -16,7 +16,7 @@
 //                   same indices, so one wave owns both halves of a SiLU pair.
 //   DN (down)     : d rows x f K, row tile q holds output features 16q..16q+15.
 //
-// Arena per layer: router wr fp32 [d,E] | bias fp32 [E] (padded) | for each
+// Arena per layer: router wrT fp32 [E,d] (transposed) | bias fp32 [E] (padded) | for each
 // local expert: GU then DN.
 #pragma once
 
@@ -148,13 +148,26 @@ struct GemmArgs {
 extern "C" {
 hipError_t moe_launch_pack(const uint16_t* src, int K, int N, void* dst, int rt_mul, int rt_add,
                            hipStream_t s);
-hipError_t moe_launch_router_partial(const uint16_t* x, const float* wr, int T, int d, int E,
-                                     int n_slices, double* partial, hipStream_t s);
-hipError_t moe_launch_route(const double* partial, const float* logits_in, const float* bias,
-                            int n_slices, int T, int E, int k, int e_begin, int n_local,
+int moe_route_small_max_tokens();
+int moe_route_decode_ok(int T, int E, int k);
+int moe_route_decode_wgs(int d);
+hipError_t moe_launch_zero_counter(unsigned int* counter, hipStream_t s);
+hipError_t moe_launch_route_decode(const uint16_t* x, const float* wrT, const float* bias,
+                                   double* partial, unsigned int* counter, int T, int d, int E,
+                                   int k, int e_begin, int n_local, int tile_rows,
+                                   const moe::RouteView* rv, hipStream_t s);
+hipError_t moe_launch_route_small(const uint16_t* x, const float* wrT, const float* bias, int T,
+                                  int d, int E, int k, int e_begin, int n_local, int tile_rows,
+                                  const moe::RouteView* rv, hipStream_t s);
+hipError_t moe_launch_router_logits(const uint16_t* x, const float* wrT, const float* bias, int T,
+                                    int d, int E, float* logits, hipStream_t s);
+hipError_t moe_launch_route(const float* logits_in, int T, int E, int k, int e_begin, int n_local,
                             int tile_rows, const moe::RouteView* rv, hipStream_t s);
-hipError_t moe_launch_decode(const moe::DecodeArgs* a, int n_slots, hipStream_t s);
-hipError_t moe_launch_prefill(const moe::GemmArgs* a, hipStream_t s);
+hipError_t moe_launch_transpose_router(const float* wr, int d, int E, float* wrT, hipStream_t s);
+hipError_t moe_launch_decode_gateup(const moe::DecodeArgs* a, int n_slots, hipStream_t s);
+hipError_t moe_launch_decode_down(const moe::DecodeArgs* a, int n_slots, hipStream_t s);
+hipError_t moe_launch_gemm_gateup(const moe::GemmArgs* a, hipStream_t s);
+hipError_t moe_launch_gemm_down(const moe::GemmArgs* a, hipStream_t s);
 hipError_t moe_prefill_set_lds_limit();
 int moe_prefill_tile_rows();
 hipError_t moe_launch_combine(const float* O, const int32_t* pair_row, const float* topk_w, int T,

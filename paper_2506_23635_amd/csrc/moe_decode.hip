@@ -125,13 +125,17 @@ __global__ __launch_bounds__(64) void down_kernel(DecodeArgs a)
 
 }  // namespace moe
 
-extern "C" hipError_t moe_launch_decode(const moe::DecodeArgs* a, int n_slots, hipStream_t s)
+extern "C" hipError_t moe_launch_decode_gateup(const moe::DecodeArgs* a, int n_slots,
+                                               hipStream_t s)
 {
-    const int gu_blocks = n_slots * (a->f / moe::kTileRows);
-    const int dn_blocks = n_slots * (a->d / moe::kTileRows);
-    hipLaunchKernelGGL(moe::gateup_kernel, dim3(gu_blocks), dim3(64), 0, s, *a);
-    hipError_t err = hipGetLastError();
-    if (err != hipSuccess) return err;
-    hipLaunchKernelGGL(moe::down_kernel, dim3(dn_blocks), dim3(64), 0, s, *a);
+    const int blocks = n_slots * (a->f / moe::kTileRows);
+    hipLaunchKernelGGL(moe::gateup_kernel, dim3(blocks), dim3(64), 0, s, *a);
+    return hipGetLastError();
+}
+
+extern "C" hipError_t moe_launch_decode_down(const moe::DecodeArgs* a, int n_slots, hipStream_t s)
+{
+    const int blocks = n_slots * (a->d / moe::kTileRows);
+    hipLaunchKernelGGL(moe::down_kernel, dim3(blocks), dim3(64), 0, s, *a);
     return hipGetLastError();
 }
