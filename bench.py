@@ -123,6 +123,10 @@ def main():
     ap.add_argument("--prefill-steps", type=int, default=20)
     ap.add_argument("--no-prefill", action="store_true")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--prefill-only", action="store_true",
+                    help="time only the prefill layer (for counter collection)")
+    ap.add_argument("--calibrate-copy", action="store_true",
+                    help="also run one 1 GiB device copy of known size (counter calibration)")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py measures one GPU only: this build has no multi-GPU path "
@@ -136,6 +140,25 @@ def main():
         sys.exit(1)
     import paper_2506_23635_amd as moe
     moe.lib()   # raises if the HIP library is not built
+
+    if args.calibrate_copy:
+        src = torch.empty(1 << 30, dtype=torch.uint8, device="cuda")
+        dst = torch.empty_like(src)
+        torch.cuda.synchronize()
+        dst.copy_(src)          # reads 1 GiB, writes 1 GiB
+        torch.cuda.synchronize()
+        del src, dst
+        torch.cuda.empty_cache()
+    if args.prefill_only:
+        pw = mi.WORKLOADS["prefill"]
+        player, px = setup_layer(pw, max_tokens=pw.T)
+        pms, pkern, prt, _ = time_layer(player, px, args.prefill_steps, 2)
+        rows = int(prt["offsets"][-1])
+        print(json.dumps({"prefill_ms": pms, "tflops": 2.0 * rows * 3 * pw.d * pw.f / (pms * 1e-3) / 1e12,
+                          "kernels_ms": {k: v["ms_per_launch"] for k, v in pkern.items()}}),
+              flush=True)
+        player.close()
+        return
 
     wl = mi.WORKLOADS["decode"]
     log("setup decode layer (16 experts, 6.3 GB) ...")
