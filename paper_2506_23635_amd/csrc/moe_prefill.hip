@@ -78,8 +78,8 @@ __device__ __forceinline__ void tile_loop(const TileCtx& c, int n_batch, uint8_t
         for (int fb = 0; fb < FB; ++fb)
 #pragma unroll
             for (int ks = 0; ks < 2; ++ks)
-                A[fb * 2 + ks] = __builtin_nontemporal_load(reinterpret_cast<const u32x4_t*>(
-                    c.a_src + fb * c.a_fstride + (uint64_t)(2 * s + ks) * kTileBytes));
+                A[fb * 2 + ks] = *reinterpret_cast<const u32x4_t*>(
+                    c.a_src + fb * c.a_fstride + (uint64_t)(2 * s + ks) * kTileBytes);
     };
     // B goes global -> LDS directly (16 bytes per lane; a wave-wide load
     // fills one 1 KiB fragment in lane order)
