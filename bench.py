@@ -86,6 +86,23 @@ def time_layer(layer, x, steps, warmup, kernel_events=True):
     return (t1 - t0) * 1e3 / steps, per_kernel, rt, dropped
 
 
+def measured_traffic(kernel="decode_gateup", source="moe_decode.hip"):
+    """HBM bytes per launch of the dominant kernel from the committed counter
+    summary (raw fabric read/write requests), or None when the kernel source
+    has changed since those counters were taken."""
+    import hashlib
+    path = os.path.join(ROOT, "profiles", "dbrx_moe_layer_counters.txt")
+    src = os.path.join(ROOT, "paper_2506_23635_amd", "csrc", source)
+    if not (os.path.exists(path) and os.path.exists(src)):
+        return None
+    digest = hashlib.sha256(open(src, "rb").read()).hexdigest()
+    for line in open(path):
+        f = line.split()
+        if len(f) >= 10 and f[0] == "traffic_bytes_per_launch" and f[1] == kernel:
+            return int(f[2]) if f[-1] == digest else None
+    return None
+
+
 def cpu_baseline(wl, budget_s=10.0):
     """The fp64 oracle on the decode token of the workload, repeated for about
     budget_s seconds of host time (weights generated before the clock)."""
@@ -235,7 +252,7 @@ def main():
         "touched_experts": touched,
         "roofline": {"bound": "hbm", "kernel": "decode_gateup", "achieved": gu_gbs,
                      "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": gu_gbs / HBM_PEAK_GBS,
-                     "traffic": None},
+                     "traffic": measured_traffic(), "algorithmic_bytes": gu_bytes},
         "kernels_us": {k: v["ms_per_launch"] * 1e3 for k, v in kern.items()},
         "ms_per_step_with_kernel_events": ms_ev,
         "profile_dropped": dropped,
