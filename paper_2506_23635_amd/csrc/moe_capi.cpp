@@ -6,6 +6,7 @@
 // once into a persistent array and indexed per layer).
 #include <hip/hip_runtime.h>
 
+#include <cstdint>
 #include <cstdio>
 #include <cstdlib>
 #include <cstring>
@@ -46,6 +47,8 @@ const char* check_config(const moe_config* c)
         return "local expert range outside [0, n_experts)";
     if (c->n_layers < 1 || c->n_layers > 1024) return "n_layers must be in [1, 1024]";
     if (c->max_tokens < 1 || c->max_tokens > (1 << 20)) return "max_tokens must be in [1, 2^20]";
+    if ((int64_t)c->max_tokens * c->d_model * 2 > INT32_MAX)
+        return "max_tokens * d_model * 2 must stay below 2^31 (32-bit gather offsets)";
     if (c->flags != 0) return "flags must be 0";
     return nullptr;
 }
@@ -269,6 +272,7 @@ moe_status run_experts(moe_ctx* ctx, int layer, const uint16_t* x, int T, hipStr
         a.d = c.d_model;
         a.f = c.ffn_dim;
         a.e_begin = c.expert_begin;
+        a.T = T;
         if (!ctx->gemm_lds_set) {
             e = moe_prefill_set_lds_limit();
             if (e != hipSuccess) return hip_fail(ctx, e, "GEMM kernel LDS attribute");

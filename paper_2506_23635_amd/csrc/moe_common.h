@@ -140,6 +140,7 @@ struct GemmArgs {
     const int32_t* tiles;     // [max_tiles][2] = (expert, first row)
     const int32_t* n_tiles;   // [1]
     int d, f, e_begin, max_tiles;
+    int T;                    // tokens of the call (rows of x)
 };
 
 }  // namespace moe

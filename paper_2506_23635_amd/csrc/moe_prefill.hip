@@ -1,23 +1,27 @@
 // moe_prefill.hip -- the expert FFN for many tokens (prefill): a grouped GEMM
-// on the bf16 matrix cores (v_mfma_f32_16x16x32_bf16).
+// on the bf16 matrix cores (v_mfma_f32_32x32x16_bf16).
 //
-// A workgroup computes a BM x BN tile of C = W X^T for one expert: W (the A
-// operand) is BM output features of the expert's packed weights, X (the B
-// operand) is BN of the expert's token rows (K contiguous).  Four waves split
-// the features (4 x 64); each wave owns a 64-feature x 256-token block, so 64
-// MFMA blocks of 16 x 16 per 32-wide K step, and each weight slab is re-read
-// by only ceil(tokens / 256) workgroups.
+// A workgroup computes a BM x BN = 256 x 256 tile of C = W X^T for one
+// expert: W (the A operand) is 256 output features of the expert's packed
+// weights, X (the B operand) is 256 of the expert's token rows (K
+// contiguous).  Four waves split the features (4 x 64); each wave owns a
+// 64-feature x 256-token block (2 x 8 MFMA blocks of 32 x 32, all 256
+// accumulator registers), so each weight slab is re-read by only
+// ceil(tokens / 256) workgroups.  One workgroup per CU (128 KiB of LDS),
+// one wave per SIMD: latency is hidden by software pipelining alone.
 //
-//  - A never touches LDS: the packed layout already holds every 16 x 32
+//  - A never touches LDS: the packed layout already holds every 32 x 16
 //    fragment as 1 KiB in lane order, each fragment is used by exactly one
 //    wave, and the wave loads it straight into registers through a ring of
-//    three K stages (two in flight while one computes).
-//  - B (the gathered token rows, shared by all four waves) is staged through
-//    double-buffered LDS in the same fragment order, loaded two stages ahead
-//    into registers, so the only LDS traffic is one 32 KiB write and four
-//    32 KiB reads per 64-wide K stage.
-//  - Token blocks past the expert's last row skip their MFMAs, so the padding
-//    waste is at most 15 rows per expert instead of a whole tile.
+//    three 64-wide K stages.
+//  - B (the gathered token rows, shared by all four waves) goes from HBM to
+//    LDS by buffer loads with the LDS-direct option, four stages deep; each
+//    load reads whole 128-byte lines and the chunks of each row are
+//    XOR-swizzled in LDS so that the fragment reads are conflict-free.  The
+//    fragments are read into a small register window a few MFMAs ahead,
+//    also across stage boundaries.
+//  - An expert's partial last token tile skips the MFMAs of token-block
+//    pairs past its last row (the padding waste is under 64 rows).
 //  - Workgroups are numbered so that consecutive tiles (same weight slab,
 //    consecutive token tiles) land on the same XCD and share its L2.
 //
@@ -34,155 +38,192 @@ namespace moe {
 
 constexpr int BM = 256;         // features per workgroup tile
 constexpr int BN = 256;         // token rows per workgroup tile
-constexpr int BK = 64;          // K per stage (two 32-K fragments)
+constexpr int BK = 64;          // K per stage (four 16-K MFMA steps)
 constexpr int kThreads = 256;   // 4 waves, one per 64-feature slab
-constexpr int FB = 4;           // 16-feature blocks per wave
-constexpr int NB = BN / 16;     // 16-token blocks per tile
-constexpr int A_STAGES = 3;     // register ring of A stages (two in flight while one computes)
-constexpr int B_FRAGS = NB * (BK / 32);           // 32 fragments of B per stage
+constexpr int FB = 2;           // 32-feature MFMA blocks per wave
+constexpr int kWaveRt = 2 * FB; // 16-row weight tiles per wave
+constexpr int TB = BN / 32;     // 32-token MFMA blocks per tile
+constexpr int KS = BK / 16;     // 16-K MFMA steps per stage
+constexpr int kRingA = 3;       // register ring of A stages
+constexpr int kRingB = 4;       // LDS ring of B stages
+constexpr int A_FRAGS = FB * KS;                  // 8 A fragments per wave per stage
+constexpr int B_FRAGS = TB * KS;                  // 32 B fragments per stage
 constexpr int B_LOADS = B_FRAGS * 64 / kThreads;  // 8 per thread
 constexpr int B_STAGE_BYTES = B_FRAGS * kTileBytes;  // 32 KiB
-constexpr int B_BUFS = 3;       // LDS ring of B stages (two in flight while one computes)
 constexpr int kXcds = 8;
-constexpr int kBBatch = 4;      // B fragments read from LDS per MFMA batch
-// s_waitcnt immediate (gfx9 layout: vmcnt[3:0] | expcnt[6:4] | lgkmcnt[11:8] |
-// vmcnt[15:14]) waiting until at most N vector-memory ops are outstanding:
-// before stage s the ops issued after B(s) are B(s+1) and A(s+1), A(s+2).
-constexpr int kAfterB = B_LOADS + 2 * (FB * 2);   // 8 + 16 = 24
+constexpr int kBufferFlags = 0x00020000;   // buffer descriptor word 3 (raw dword data, gfx9 family)
 constexpr int kWaitAll = (0x7 << 4) | (0xF << 8);   // vmcnt 0
+// s_waitcnt immediate (gfx9 layout: vmcnt[3:0] | expcnt[6:4] | lgkmcnt[11:8] |
+// vmcnt[15:14]) waiting until at most N vector-memory ops are outstanding.
+// Stage t issues B(t+RB-1) at its barrier and A(t+RA) at its end, so at
+// stage s's barrier the ops issued after B(s+1) are the A loads of stages
+// s-RB+2 .. s-1 and B(s+2) .. B(s+RB-2); vector-memory ops complete in order.
+constexpr int kAfterB = (kRingB - 3) * B_LOADS + (kRingB - 2) * A_FRAGS;
+static_assert(kAfterB < 64, "vmcnt holds 6 bits");
+static_assert(kRingA == 3, "the K loop is unrolled by three stages");
 constexpr int kWaitBStage = (kAfterB & 0xF) | ((kAfterB >> 4) << 14) | (0x7 << 4) | (0xF << 8);
+
+typedef __attribute__((__vector_size__(16 * sizeof(float)))) float f32x16_t;
+
+__device__ inline f32x16_t mfma32x32x16(const u32x4_t a, const u32x4_t b, f32x16_t c)
+{
+    return __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8_t, a),
+                                                   __builtin_bit_cast(bf16x8_t, b), c, 0, 0, 0);
+}
 
 enum { kGateUp = 0, kDown = 1 };
 
+#ifndef MOE_B_SWZ_SHIFT
+#define MOE_B_SWZ_SHIFT 0
+#endif
+// chunk swizzle of B row R in LDS (a function of R mod 16 only, so 32-row
+// token blocks share it)
+__device__ __forceinline__ int b_swizzle(int R) { return (R >> MOE_B_SWZ_SHIFT) & 7; }
+
 struct TileCtx {
-    const uint8_t* a_src;      // this lane's first A fragment (stage 0, ks 0)
-    uint64_t a_fstride;        // bytes between 16-feature blocks
-    const uint16_t* b_base;    // x (gathered) or H
-    uint32_t b_off[B_LOADS];   // element offsets of this thread's B rows
+    const uint8_t* a_src;      // this lane's A bytes for feature block 0, stage 0, step 0
+    uint64_t a_fstride;        // bytes between 32-feature blocks (two row tiles)
+    __amdgpu_buffer_rsrc_t b_rsrc;  // buffer over x (gate/up) or over the tile's rows of H
+    uint32_t b_off[B_LOADS];   // byte offsets in b_rsrc of this lane's 16-byte chunk, per load
+    uint32_t rd_off[KS];       // LDS byte offsets of this lane's B fragment piece, per K step
     int n_stages;
     int w, lane;
 };
 
-// The K loop of one tile.  Token blocks go in batches of kBBatch; only the
-// first n_batch batches (those holding rows of the tile) run their MFMAs, and
-// the check is one uniform branch per batch of 16 MFMAs.
-__device__ __forceinline__ void tile_loop(const TileCtx& c, int n_batch, uint8_t* lds,
-                                          f32x4_t (&acc)[FB][NB])
+// The K loop of one tile on v_mfma_f32_32x32x16_bf16.  A 32 x 16 operand
+// fragment is 1 KiB in lane order (lane l: row l%32, K 8(l/32)..+7).
+//
+// A stage is 32 units (16-K step j, 32-token block t), j-major; a unit is
+// one B fragment read from LDS and the two MFMAs (both feature blocks) that
+// use it.  B fragments are read kLook units ahead through a small register
+// window, also across stage boundaries: the barrier that publishes the next
+// stage's B sits kLook units before the end of the current stage.
+// kFull: every token block holds rows (branch-free loop); otherwise only the
+// first n_pairs pairs of token blocks run their MFMAs.
+constexpr int kUnits = KS * TB;   // 32 units per stage
+constexpr int kLook = 3;          // B fragments in flight ahead of their MFMAs
+constexpr int kWin = kLook + 1;   // B register window
+static_assert(kUnits % kWin == 0, "the window index must repeat per stage");
+
+template <bool kFull>
+__device__ __forceinline__ void tile_loop(const TileCtx& c, int n_pairs, uint8_t* lds,
+                                          f32x16_t (&acc)[FB][TB])
 {
-    constexpr int kNb = NB;
     const int n_stages = c.n_stages;
     const int w = c.w, lane = c.lane;
-    u32x4_t ra[A_STAGES][FB * 2];
-    auto load_a = [&](int s, u32x4_t (&A)[FB * 2]) {
+    u32x4_t ra[kRingA][A_FRAGS];
+    u32x4_t bw[kWin];
+    // A: K step j of stage s lives in K tile 2s + j/2, second half of the
+    // tile for odd j (512 bytes on)
+    auto load_a = [&](int s, u32x4_t (&A)[A_FRAGS]) {
 #pragma unroll
         for (int fb = 0; fb < FB; ++fb)
 #pragma unroll
-            for (int ks = 0; ks < 2; ++ks)
-                A[fb * 2 + ks] = *reinterpret_cast<const u32x4_t*>(
-                    c.a_src + fb * c.a_fstride + (uint64_t)(2 * s + ks) * kTileBytes);
+            for (int j = 0; j < KS; ++j)
+                A[fb * KS + j] = *reinterpret_cast<const u32x4_t*>(
+                    c.a_src + fb * c.a_fstride + (uint64_t)(2 * s + j / 2) * kTileBytes +
+                    (j % 2) * (kTileBytes / 2));
     };
-    // B goes global -> LDS directly (16 bytes per lane; a wave-wide load
-    // fills one 1 KiB fragment in lane order)
+    // B goes global -> LDS directly through buffer loads: a stage of B is
+    // 256 rows x 128 bytes (64 K), row-major in LDS with the eight 16-byte
+    // chunks of each row XOR-swizzled (see process_tile).  Load q of wave w
+    // fills rows 64w + 8q .. +7, so every load reads whole 128-byte lines.
+    // Buffer (not global) loads: the compiler counts them in vmcnt only, so
+    // the LDS reads of the B window keep exact lgkmcnt waits.
     auto load_b = [&](int s, int buf) {
 #pragma unroll
-        for (int i = 0; i < B_LOADS; ++i)
-            __builtin_amdgcn_global_load_lds(
-                (__attribute__((address_space(1))) const void*)(c.b_base + c.b_off[i] + s * BK),
+        for (int q = 0; q < B_LOADS; ++q)
+            __builtin_amdgcn_raw_ptr_buffer_load_lds(
+                c.b_rsrc,
                 (__attribute__((address_space(3))) void*)(&lds[buf * B_STAGE_BYTES +
-                                                               (w + 4 * i) * kTileBytes]),
-                16, 0, 0);
+                                                               (w * B_LOADS + q) * kTileBytes]),
+                16, c.b_off[q], (uint32_t)s * (BK * 2), 0, 0);
     };
-    // B fragments are read from LDS in batches of kBBatch, one batch ahead of
-    // the MFMAs that use it (sched_barrier keeps the scheduler from hoisting
-    // more reads than that and running out of registers)
-    constexpr int kBatches = 2 * (kNb / kBBatch);   // (K half, token batch) pairs
-    auto batch_on = [&](int bi) { return (bi % (kNb / kBBatch)) < n_batch; };
-    auto read_batch = [&](int buf, int bi, u32x4_t (&B)[kBBatch]) {
-        const int ks = bi / (kNb / kBBatch);
-        const int nh = (bi % (kNb / kBBatch)) * kBBatch;
-#pragma unroll
-        for (int q = 0; q < kBBatch; ++q)
-            B[q] = *reinterpret_cast<const u32x4_t*>(
-                &lds[buf * B_STAGE_BYTES + ((nh + q) * 2 + ks) * kTileBytes + lane * 16]);
+    // the B fragment of unit u: token block t (rows 32t..), K step j
+    auto read_unit = [&](const uint8_t* bbuf, int u) {
+        const int j = u / TB, t = u % TB;
+        bw[u % kWin] = *reinterpret_cast<const u32x4_t*>(&bbuf[c.rd_off[j] + t * 32 * (BK * 2)]);
     };
-    auto compute = [&](int buf, const u32x4_t (&A)[FB * 2]) {
-        u32x4_t bb[2][kBBatch];
-        read_batch(buf, 0, bb[0]);
-#pragma unroll
-        for (int bi = 0; bi < kBatches; ++bi) {
-            if (bi + 1 < kBatches) read_batch(buf, bi + 1, bb[(bi + 1) & 1]);
-            __builtin_amdgcn_sched_barrier(0);
-            const int ks = bi / (kNb / kBBatch);
-            const int nh = (bi % (kNb / kBBatch)) * kBBatch;
-            if (batch_on(bi)) {
-#pragma unroll
-                for (int q = 0; q < kBBatch; ++q)
-#pragma unroll
-                    for (int fb = 0; fb < FB; ++fb)
-                        acc[fb][nh + q] =
-                            mfma16x16x32(A[fb * 2 + ks], bb[bi & 1][q], acc[fb][nh + q]);
-            }
-            __builtin_amdgcn_sched_barrier(0);
-        }
-    };
-
-    // prologue: A stages 0..2 in registers, B stages 0..1 in LDS, in flight
-    load_b(0, 0);
-    load_a(0, ra[0]);
-    load_b(1, 1);
-    load_a(1, ra[1]);
-    load_a(2, ra[2]);
-    // One iteration = three stages, so that both rings are indexed
-    // statically.  Before stage s: wait for this wave's B(s) (everything but
-    // the B(s+1), A(s+1), A(s+2) issued after it) and barrier, so every
-    // wave's B(s) is in LDS and every wave is done reading B(s-1)'s buffer;
-    // then issue B(s+2) into that buffer, compute stage s, refill ra[s % 3]
-    // with A(s+3).  Loads past the last stage re-read the last stage.
-    auto step = [&](int s, u32x4_t (&A)[FB * 2], int buf) {
-        // explicit partial wait + bare barrier: a __syncthreads() release
-        // fence would wait for every outstanding LDS DMA (vmcnt 0); the empty
-        // asm statements keep the compiler from moving memory operations
-        // across the barrier
+    // explicit partial wait + bare barrier: a __syncthreads() release fence
+    // would wait for every outstanding LDS DMA (vmcnt 0); the empty asm
+    // statements keep the compiler from moving memory operations across it
+    auto wait_and_barrier = [&]() {
         __builtin_amdgcn_s_waitcnt(kWaitBStage);
         asm volatile("" ::: "memory");
         __builtin_amdgcn_s_barrier();
         asm volatile("" ::: "memory");
-        load_b(min(s + 2, n_stages - 1), (buf + 2) % 3);
-        compute(buf, A);
-        load_a(min(s + 3, n_stages - 1), A);
     };
-    int s = 0;
-    for (; s + 3 <= n_stages; s += 3) {
-        step(s + 0, ra[0], 0);
-        step(s + 1, ra[1], 1);
-        step(s + 2, ra[2], 2);
+    // stage s (A in A, B in LDS buffer s % RB).  At unit kUnits - kLook:
+    // wait for this wave's part of B(s+1), barrier (every wave's B(s+1) is
+    // in LDS; every wave is done with buffer (s-1) % RB), issue B(s+RB-1)
+    // into that buffer, and start reading stage s+1.  After the last MFMA,
+    // refill A with A(s+RA).  Loads past the last stage re-read the last
+    // stage.
+    auto stage = [&](int s, u32x4_t (&A)[A_FRAGS]) {
+        const uint8_t* bcur = lds + (s % kRingB) * B_STAGE_BYTES;
+        const uint8_t* bnext = lds + ((s + 1) % kRingB) * B_STAGE_BYTES;
+#pragma unroll
+        for (int u = 0; u < kUnits; ++u) {
+            if (u == kUnits - kLook) {
+                wait_and_barrier();
+                load_b(min(s + kRingB - 1, n_stages - 1), (s + kRingB - 1) % kRingB);
+            }
+            if (u + kLook < kUnits)
+                read_unit(bcur, u + kLook);
+            else
+                read_unit(bnext, u + kLook - kUnits);
+            __builtin_amdgcn_sched_barrier(0);
+            const int j = u / TB, t = u % TB;
+            if (kFull || t / 2 < n_pairs) {
+#pragma unroll
+                for (int fb = 0; fb < FB; ++fb)
+                    acc[fb][t] = mfma32x32x16(A[fb * KS + j], bw[u % kWin], acc[fb][t]);
+            }
+            __builtin_amdgcn_sched_barrier(0);
+        }
+        load_a(min(s + kRingA, n_stages - 1), A);
+    };
+
+    // prologue: B stages 0..RB-2 and A stages 0..RA-1 in flight; wait for
+    // them, then read the first kLook units of stage 0 (the loads of every
+    // stage run in order: stage 0 publishes B(1) and issues B(RB-1))
+    static_assert(kRingB - 1 >= kRingA - 1, "prologue issues B ahead of A");
+#pragma unroll
+    for (int i = 0; i < kRingB - 1; ++i) {
+        load_b(min(i, n_stages - 1), i);
+        if (i < kRingA) load_a(min(i, n_stages - 1), ra[i]);
     }
-    if (s < n_stages) step(s++, ra[0], 0);
-    if (s < n_stages) step(s++, ra[1], 1);
-    // the last steps re-issued dummy B loads into LDS: drain them before the
+    __builtin_amdgcn_s_waitcnt(kWaitAll);
+    __builtin_amdgcn_s_barrier();
+    asm volatile("" ::: "memory");
+#pragma unroll
+    for (int u = 0; u < kLook; ++u) read_unit(lds, u);
+    // RA stages per iteration, so that the A ring is indexed statically
+    int s = 0;
+    for (; s + kRingA <= n_stages; s += kRingA) {
+        stage(s + 0, ra[0]);
+        stage(s + 1, ra[1]);
+        stage(s + 2, ra[2]);
+    }
+    if (s < n_stages) {
+        stage(s, ra[0]);
+        if (s + 1 < n_stages) stage(s + 1, ra[1]);
+    }
+    // the last stages re-issued dummy B loads into LDS: drain them before the
     // workgroup can finish and its LDS be handed to another workgroup
     __builtin_amdgcn_s_waitcnt(kWaitAll);
     __builtin_amdgcn_s_barrier();
 }
 
+// One BM x BN tile (feature tile ft, token tile tt) of the grouped GEMM.
 template <int kMode>
-__global__ __launch_bounds__(kThreads) void gemm_kernel(GemmArgs a)
+__device__ __forceinline__ void process_tile(const GemmArgs& a, int ft, int tt, uint8_t* lds)
 {
-    __shared__ __attribute__((aligned(16))) uint8_t lds[B_BUFS * B_STAGE_BYTES];
     const int M = kMode == kGateUp ? 2 * a.f : a.d;    // a multiple of 128
-    const int n_ftiles = (M + BM - 1) / BM;
-    // XCD-aware numbering: hardware hands block b to XCD b % 8; give each XCD
-    // a contiguous run of logical tiles (token tile fastest, so the tiles
-    // that share a weight slab run together on one XCD).
-    const int per_xcd = gridDim.x / kXcds;
-    const int logical = (blockIdx.x % kXcds) * per_xcd + blockIdx.x / kXcds;
-    const int ft = logical / a.max_tiles;
-    const int tt = logical % a.max_tiles;
-    if (ft >= n_ftiles || tt >= *a.n_tiles) return;
     const int e = a.tiles[2 * tt];
     const int row_start = a.tiles[2 * tt + 1];
     const int row_end = min(row_start + BN, a.offsets[e + 1]);
-    const int nbv = (row_end - row_start + 15) / 16;   // token blocks with rows
+    const int ntb = (row_end - row_start + 31) / 32;   // 32-token blocks with rows
 
     const int K = kMode == kGateUp ? a.d : a.f;
     const uint64_t KT = (uint64_t)K / kTileK;
@@ -196,87 +237,137 @@ __global__ __launch_bounds__(kThreads) void gemm_kernel(GemmArgs a)
     const int lane = c.lane, w = c.w;
     // a wave past M (partial last feature tile) recomputes the last valid
     // slab, keeping every load unconditional, and skips its stores
-    const bool wave_on = (uint64_t)ft * (BM / 16) + w * FB < (uint64_t)(M / 16);
-    const uint64_t rt0 = wave_on ? (uint64_t)ft * (BM / 16) + w * FB : (uint64_t)(M / 16 - FB);
-    // A: fragment (fb, ks) of stage s at a_src + fb * a_fstride + (2s + ks) KiB
-    c.a_src = wbase + tile_offset(rt0, 0, KT) + lane * 16;
-    c.a_fstride = KT * kTileBytes;
-    // B: this thread's fragments fr = w + 4 i -> (token block fr / 2, K half
-    // fr % 2), held as 32-bit element offsets into x (gathered) or H
-    c.b_base = kMode == kGateUp ? a.x : a.H;
+    const bool wave_on = (uint64_t)ft * (BM / 16) + w * kWaveRt < (uint64_t)(M / 16);
+    const uint64_t rt0 =
+        wave_on ? (uint64_t)ft * (BM / 16) + w * kWaveRt : (uint64_t)(M / 16 - kWaveRt);
+    // A: lane l of a 32 x 16 fragment reads row l%32 of the block (row tile
+    // rt0 + 2 fb + (l%32)/16, granule row l%16) at K group l/32 of the step
+    c.a_src = wbase + tile_offset(rt0 + ((lane & 31) >> 4), 0, KT) +
+              (((lane >> 5) * 16) + (lane & 15)) * 16;
+    c.a_fstride = 2 * KT * kTileBytes;
+    // B: a stage holds, for each of the 256 token rows R of the tile, the
+    // 128 bytes of K [64 s, 64 s + 64) as eight 16-byte chunks; chunk c sits
+    // in slot c ^ swz(R) so that the MFMA reads (8 consecutive rows at one
+    // chunk) fall in distinct LDS banks.  Load q of wave w: lane l reads row
+    // R = 64w + 8q + l/8, slot l%8, i.e. chunk (l%8) ^ swz(R).  Gate/up
+    // gathers rows of x (the library caps T*d*2 below 2^31, so byte offsets
+    // fit 32 bits); down reads the tile's own rows of H through a buffer
+    // based at the tile's first row.  The buffer size bounds every load
+    // (out-of-range reads return zero).
+    if (kMode == kGateUp)
+        c.b_rsrc = __builtin_amdgcn_make_buffer_rsrc(const_cast<uint16_t*>(a.x), 0,
+                                                     a.T * a.d * 2, kBufferFlags);
+    else
+        c.b_rsrc = __builtin_amdgcn_make_buffer_rsrc(a.H + (int64_t)row_start * a.f, 0,
+                                                     (row_end - row_start) * a.f * 2, kBufferFlags);
 #pragma unroll
-    for (int i = 0; i < B_LOADS; ++i) {
-        const int fr = w + 4 * i;
-        const int row = row_start + (fr / 2) * 16 + (lane & 15);
+    for (int q = 0; q < B_LOADS; ++q) {
+        const int R = w * 64 + q * 8 + (lane >> 3);
+        const int row = row_start + R;
         const int rr = row < row_end ? row : row_start;   // rows past the end: any valid row
-        const int kofs = (fr % 2) * 32 + (lane >> 4) * 8;
+        const uint32_t chunk = (uint32_t)((lane & 7) ^ b_swizzle(R)) * 16;
         if (kMode == kGateUp)
-            c.b_off[i] = (uint32_t)a.row_token[rr] * (uint32_t)a.d + kofs;
+            c.b_off[q] = (uint32_t)a.row_token[rr] * (uint32_t)a.d * 2 + chunk;
         else
-            c.b_off[i] = (uint32_t)rr * (uint32_t)a.f + kofs;
+            c.b_off[q] = (uint32_t)(rr - row_start) * (uint32_t)a.f * 2 + chunk;
+    }
+    // MFMA B operand of K step j, token block t: lane l takes row
+    // R = 32t + l%32, chunk 2j + l/32 (swz(R) does not depend on t)
+#pragma unroll
+    for (int j = 0; j < KS; ++j) {
+        const int R = lane & 31;
+        c.rd_off[j] = (uint32_t)R * (BK * 2) + (uint32_t)(((2 * j + (lane >> 5)) ^ b_swizzle(R)) * 16);
     }
 
-    f32x4_t acc[FB][NB];
+    f32x16_t acc[FB][TB];
 #pragma unroll
     for (int fb = 0; fb < FB; ++fb)
 #pragma unroll
-        for (int nb = 0; nb < NB; ++nb) acc[fb][nb] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+        for (int tb = 0; tb < TB; ++tb) acc[fb][tb] = f32x16_t{};
 
-    tile_loop(c, (nbv + kBBatch - 1) / kBBatch, lds, acc);
+    // full tiles take the branch-free loop; an expert's partial last tile
+    // skips the MFMAs of token-block pairs past its last row
+    if (ntb == TB)
+        tile_loop<true>(c, TB / 2, lds, acc);
+    else
+        tile_loop<false>(c, (ntb + 1) / 2, lds, acc);
 
-    // epilogue: lane holds features 4*(lane/16)+r of token column lane%16
+    // epilogue: in a 32 x 32 block lane l holds token column l%32 and rows
+    // 8g + 4(l/32) + r in register 4g + r (g, r = 0..3).  A 32-row block is
+    // row tiles (rt, rt + 1): for the gate/up GEMM that is 16 gate rows
+    // (g = 0, 1) and the 16 up rows of the same features (g = 2, 3).
     if (!wave_on) return;
-    const int g = lane >> 4;
-    const int jcol = lane & 15;
+    const int half = lane >> 5;
+    const int jcol = lane & 31;
 #pragma unroll
-    for (int nb = 0; nb < NB; ++nb) {
-        const int row = row_start + nb * 16 + jcol;
+    for (int tb = 0; tb < TB; ++tb) {
+        const int row = row_start + tb * 32 + jcol;
         if (row >= row_end) continue;
-        if (kMode == kGateUp) {
 #pragma unroll
-            for (int fb = 0; fb < FB; fb += 2) {
-                const f32x4_t gg = acc[fb][nb], uu = acc[fb + 1][nb];
-                const int feat = (int)((rt0 + fb) / 2) * 16 + g * 4;
-                uint32_t h01 = (uint32_t)f32_to_bf16(silu_mul(gg[0], uu[0])) |
-                               ((uint32_t)f32_to_bf16(silu_mul(gg[1], uu[1])) << 16);
-                uint32_t h23 = (uint32_t)f32_to_bf16(silu_mul(gg[2], uu[2])) |
-                               ((uint32_t)f32_to_bf16(silu_mul(gg[3], uu[3])) << 16);
-                *reinterpret_cast<uint2*>(a.H + (int64_t)row * a.f + feat) = make_uint2(h01, h23);
-            }
-        } else {
+        for (int fb = 0; fb < FB; ++fb) {
+            const f32x16_t v = acc[fb][tb];
+            const uint64_t rt = rt0 + 2 * fb;
+            if (kMode == kGateUp) {
 #pragma unroll
-            for (int fb = 0; fb < FB; ++fb) {
-                const f32x4_t o = acc[fb][nb];
-                const int feat = (int)(rt0 + fb) * 16 + g * 4;
-                *reinterpret_cast<float4*>(a.O + (int64_t)row * a.d + feat) =
-                    make_float4(o[0], o[1], o[2], o[3]);
+                for (int g = 0; g < 2; ++g) {
+                    const int feat = (int)(rt / 2) * 16 + 8 * g + 4 * half;
+                    uint32_t h01 = (uint32_t)f32_to_bf16(silu_mul(v[4 * g + 0], v[4 * g + 8])) |
+                                   ((uint32_t)f32_to_bf16(silu_mul(v[4 * g + 1], v[4 * g + 9])) << 16);
+                    uint32_t h23 = (uint32_t)f32_to_bf16(silu_mul(v[4 * g + 2], v[4 * g + 10])) |
+                                   ((uint32_t)f32_to_bf16(silu_mul(v[4 * g + 3], v[4 * g + 11])) << 16);
+                    *reinterpret_cast<uint2*>(a.H + (int64_t)row * a.f + feat) = make_uint2(h01, h23);
+                }
+            } else {
+#pragma unroll
+                for (int g = 0; g < 4; ++g) {
+                    const int feat = (int)rt * 16 + 8 * g + 4 * half;
+                    *reinterpret_cast<float4*>(a.O + (int64_t)row * a.d + feat) =
+                        make_float4(v[4 * g], v[4 * g + 1], v[4 * g + 2], v[4 * g + 3]);
+                }
             }
         }
     }
+}
+
+template <int kMode>
+__global__ __launch_bounds__(kThreads) void gemm_kernel(GemmArgs a)
+{
+    __shared__ __attribute__((aligned(16))) uint8_t lds[kRingB * B_STAGE_BYTES];
+    const int M = kMode == kGateUp ? 2 * a.f : a.d;
+    const int n_ftiles = (M + BM - 1) / BM;
+    // XCD-aware numbering: hardware hands block b to XCD b % 8; give each XCD
+    // a contiguous run of logical tiles (token tile fastest, so the tiles
+    // that share a weight slab run together on one XCD).
+    const int per_xcd = gridDim.x / kXcds;
+    const int logical = (blockIdx.x % kXcds) * per_xcd + blockIdx.x / kXcds;
+    const int ft = logical / a.max_tiles;
+    const int tt = logical % a.max_tiles;
+    if (ft >= n_ftiles || tt >= *a.n_tiles) return;
+    process_tile<kMode>(a, ft, tt, lds);
 }
 
 }  // namespace moe
 
 extern "C" int moe_prefill_tile_rows() { return moe::BN; }
 
-static int gemm_grid(int n_ftiles, int max_tiles)
+template <int kMode>
+static hipError_t launch_gemm(const moe::GemmArgs* a, hipStream_t s)
 {
-    const int n = n_ftiles * max_tiles;
-    return (n + moe::kXcds - 1) / moe::kXcds * moe::kXcds;
+    const int M = kMode == moe::kGateUp ? 2 * a->f : a->d;
+    const int n = (M + moe::BM - 1) / moe::BM * a->max_tiles;
+    const int grid = (n + moe::kXcds - 1) / moe::kXcds * moe::kXcds;
+    hipLaunchKernelGGL((moe::gemm_kernel<kMode>), dim3(grid), dim3(moe::kThreads), 0, s, *a);
+    return hipGetLastError();
 }
 
 extern "C" hipError_t moe_launch_gemm_gateup(const moe::GemmArgs* a, hipStream_t s)
 {
-    const int grid = gemm_grid((2 * a->f + moe::BM - 1) / moe::BM, a->max_tiles);
-    hipLaunchKernelGGL(moe::gemm_kernel<moe::kGateUp>, dim3(grid), dim3(moe::kThreads), 0, s, *a);
-    return hipGetLastError();
+    return launch_gemm<moe::kGateUp>(a, s);
 }
 
 extern "C" hipError_t moe_launch_gemm_down(const moe::GemmArgs* a, hipStream_t s)
 {
-    const int grid = gemm_grid((a->d + moe::BM - 1) / moe::BM, a->max_tiles);
-    hipLaunchKernelGGL(moe::gemm_kernel<moe::kDown>, dim3(grid), dim3(moe::kThreads), 0, s, *a);
-    return hipGetLastError();
+    return launch_gemm<moe::kDown>(a, s);
 }
 
 extern "C" hipError_t moe_prefill_set_lds_limit() { return hipSuccess; }

@@ -41,6 +41,11 @@ def dbrx(**kw):
     return moe.make_config(**base)
 
 
+def test_largest_max_tokens_accepted():
+    # 174762 tokens of 6144 bf16 values stay below 2^31 bytes
+    assert moe.moe_workspace_bytes(dbrx(max_tokens=174762)) > 0
+
+
 def test_weight_bytes_formula():
     cfg = dbrx()
     expert = 3 * 6144 * 10752 * 2
@@ -54,8 +59,10 @@ def test_weight_bytes_formula():
 @pytest.mark.parametrize("bad", [dict(d_model=100), dict(d_model=0), dict(ffn_dim=96),
                                  dict(n_experts=0), dict(n_experts=65), dict(top_k=0),
                                  dict(top_k=17), dict(expert_begin=13, n_local_experts=4),
-                                 dict(n_layers=0), dict(max_tokens=0), dict(flags=1)])
+                                 dict(n_layers=0), dict(max_tokens=0), dict(flags=1),
+                                 dict(max_tokens=174763)])
 def test_bad_configs_rejected(bad):
+    # max_tokens 174763: x is then 2^31 bytes or more, past the GEMM's 32-bit gather offsets
     cfg = dbrx(**bad)
     if bad.get("n_experts") == 0:
         cfg.n_local_experts = 0
