@@ -53,15 +53,8 @@ constexpr int B_STAGE_BYTES = B_FRAGS * kTileBytes;  // 32 KiB
 constexpr int kXcds = 8;
 constexpr int kBufferFlags = 0x00020000;   // buffer descriptor word 3 (raw dword data, gfx9 family)
 constexpr int kWaitAll = (0x7 << 4) | (0xF << 8);   // vmcnt 0
-// s_waitcnt immediate (gfx9 layout: vmcnt[3:0] | expcnt[6:4] | lgkmcnt[11:8] |
-// vmcnt[15:14]) waiting until at most N vector-memory ops are outstanding.
-// Stage t issues B(t+RB-1) at its barrier and A(t+RA) at its end, so at
-// stage s's barrier the ops issued after B(s+1) are the A loads of stages
-// s-RB+2 .. s-1 and B(s+2) .. B(s+RB-2); vector-memory ops complete in order.
-constexpr int kAfterB = (kRingB - 3) * B_LOADS + (kRingB - 2) * A_FRAGS;
-static_assert(kAfterB < 64, "vmcnt holds 6 bits");
 static_assert(kRingA == 3, "the K loop is unrolled by three stages");
-constexpr int kWaitBStage = (kAfterB & 0xF) | ((kAfterB >> 4) << 14) | (0x7 << 4) | (0xF << 8);
+static_assert(kRingB == 4, "stage s reads B(s), publishes B(s+1), loads B(s+2)");
 
 typedef __attribute__((__vector_size__(16 * sizeof(float)))) float f32x16_t;
 
@@ -73,12 +66,19 @@ __device__ inline f32x16_t mfma32x32x16(const u32x4_t a, const u32x4_t b, f32x16
 
 enum { kGateUp = 0, kDown = 1 };
 
-#ifndef MOE_B_SWZ_SHIFT
-#define MOE_B_SWZ_SHIFT 0
+#ifndef MOE_B_SWZ
+#define MOE_B_SWZ 2
 #endif
 // chunk swizzle of B row R in LDS (a function of R mod 16 only, so 32-row
-// token blocks share it)
-__device__ __forceinline__ int b_swizzle(int R) { return (R >> MOE_B_SWZ_SHIFT) & 7; }
+// token blocks share it): rows 0..7 take eight distinct slots, and rows
+// 8..15 the complementary (row parity, slot) pairs, so any 8 consecutive
+// rows or 16 consecutive rows at one chunk hit distinct banks
+__device__ __forceinline__ int b_swizzle(int R)
+{
+    if (MOE_B_SWZ == 0) return R & 7;
+    if (MOE_B_SWZ == 1) return (R >> 1) & 7;
+    return (R & 7) ^ ((R >> 3) & 1);
+}
 
 struct TileCtx {
     const uint8_t* a_src;      // this lane's A bytes for feature block 0, stage 0, step 0
@@ -98,12 +98,50 @@ struct TileCtx {
 // use it.  B fragments are read kLook units ahead through a small register
 // window, also across stage boundaries: the barrier that publishes the next
 // stage's B sits kLook units before the end of the current stage.
+//
+// The global loads are spread over the units (a burst of them would stall
+// the wave's in-order issue behind the address unit): stage s issues load q
+// of B(s+2) at unit 4q + 1 (into the LDS buffer that stage s-2 used, free
+// since stage s-1's barrier), and refills A fragment (fb, j) with A(s+3) two
+// units after the last MFMA that reads it.
 // kFull: every token block holds rows (branch-free loop); otherwise only the
 // first n_pairs pairs of token blocks run their MFMAs.
 constexpr int kUnits = KS * TB;   // 32 units per stage
 constexpr int kLook = 3;          // B fragments in flight ahead of their MFMAs
 constexpr int kWin = kLook + 1;   // B register window
+constexpr int kBarrierUnit = kUnits - kLook;
 static_assert(kUnits % kWin == 0, "the window index must repeat per stage");
+static_assert(kUnits == 4 * B_LOADS, "one B load every four units");
+
+// the unit at which stage s issues B load q of B(s+2)
+constexpr int b_load_unit(int q) { return 4 * q + 1; }
+// the unit at which stage s refills A fragment (fb, j) with A(s+3): the
+// units of K step j are 8j .. 8j+7; the last K step's fragments go after
+// the stage (unit kUnits)
+constexpr int a_load_unit(int fb, int j) { return j + 1 < KS ? 8 * (j + 1) + 2 * fb : kUnits; }
+// vector-memory ops issued after the last load of B(s+1) (stage s-1, unit
+// b_load_unit(B_LOADS-1)) up to stage s's barrier; vector-memory ops
+// complete in order, so waiting until at most this many are outstanding
+// means this wave's part of B(s+1) is in LDS
+constexpr int vm_after_last_b()
+{
+    int n = 0;
+    for (int fb = 0; fb < FB; ++fb)
+        for (int j = 0; j < KS; ++j) {
+            const int u = a_load_unit(fb, j);
+            if (u > b_load_unit(B_LOADS - 1)) ++n;   // rest of stage s-1
+            if (u < kBarrierUnit) ++n;               // stage s before the barrier
+        }
+    for (int q = 0; q < B_LOADS; ++q)
+        if (b_load_unit(q) < kBarrierUnit) ++n;
+    return n;
+}
+constexpr int kAfterB = vm_after_last_b();
+static_assert(b_load_unit(B_LOADS - 1) >= kBarrierUnit, "every B(s+1) load precedes the count");
+static_assert(kAfterB < 64, "vmcnt holds 6 bits");
+// s_waitcnt immediate (gfx9 layout: vmcnt[3:0] | expcnt[6:4] | lgkmcnt[11:8] |
+// vmcnt[15:14])
+constexpr int kWaitBStage = (kAfterB & 0xF) | ((kAfterB >> 4) << 14) | (0x7 << 4) | (0xF << 8);
 
 template <bool kFull>
 __device__ __forceinline__ void tile_loop(const TileCtx& c, int n_pairs, uint8_t* lds,
@@ -113,16 +151,12 @@ __device__ __forceinline__ void tile_loop(const TileCtx& c, int n_pairs, uint8_t
     const int w = c.w, lane = c.lane;
     u32x4_t ra[kRingA][A_FRAGS];
     u32x4_t bw[kWin];
-    // A: K step j of stage s lives in K tile 2s + j/2, second half of the
-    // tile for odd j (512 bytes on)
-    auto load_a = [&](int s, u32x4_t (&A)[A_FRAGS]) {
-#pragma unroll
-        for (int fb = 0; fb < FB; ++fb)
-#pragma unroll
-            for (int j = 0; j < KS; ++j)
-                A[fb * KS + j] = *reinterpret_cast<const u32x4_t*>(
-                    c.a_src + fb * c.a_fstride + (uint64_t)(2 * s + j / 2) * kTileBytes +
-                    (j % 2) * (kTileBytes / 2));
+    // A fragment (fb, j) of stage s: K step j lives in K tile 2s + j/2,
+    // second half of the tile for odd j (512 bytes on)
+    auto load_a1 = [&](int s, int fb, int j, u32x4_t& dst) {
+        dst = *reinterpret_cast<const u32x4_t*>(c.a_src + fb * c.a_fstride +
+                                                (uint64_t)(2 * s + j / 2) * kTileBytes +
+                                                (j % 2) * (kTileBytes / 2));
     };
     // B goes global -> LDS directly through buffer loads: a stage of B is
     // 256 rows x 128 bytes (64 K), row-major in LDS with the eight 16-byte
@@ -130,14 +164,12 @@ __device__ __forceinline__ void tile_loop(const TileCtx& c, int n_pairs, uint8_t
     // fills rows 64w + 8q .. +7, so every load reads whole 128-byte lines.
     // Buffer (not global) loads: the compiler counts them in vmcnt only, so
     // the LDS reads of the B window keep exact lgkmcnt waits.
-    auto load_b = [&](int s, int buf) {
-#pragma unroll
-        for (int q = 0; q < B_LOADS; ++q)
-            __builtin_amdgcn_raw_ptr_buffer_load_lds(
-                c.b_rsrc,
-                (__attribute__((address_space(3))) void*)(&lds[buf * B_STAGE_BYTES +
-                                                               (w * B_LOADS + q) * kTileBytes]),
-                16, c.b_off[q], (uint32_t)s * (BK * 2), 0, 0);
+    auto load_b1 = [&](int s, int buf, int q) {
+        __builtin_amdgcn_raw_ptr_buffer_load_lds(
+            c.b_rsrc,
+            (__attribute__((address_space(3))) void*)(&lds[buf * B_STAGE_BYTES +
+                                                           (w * B_LOADS + q) * kTileBytes]),
+            16, c.b_off[q], (uint32_t)s * (BK * 2), 0, 0);
     };
     // the B fragment of unit u: token block t (rows 32t..), K step j
     auto read_unit = [&](const uint8_t* bbuf, int u) {
@@ -153,21 +185,22 @@ __device__ __forceinline__ void tile_loop(const TileCtx& c, int n_pairs, uint8_t
         __builtin_amdgcn_s_barrier();
         asm volatile("" ::: "memory");
     };
-    // stage s (A in A, B in LDS buffer s % RB).  At unit kUnits - kLook:
-    // wait for this wave's part of B(s+1), barrier (every wave's B(s+1) is
-    // in LDS; every wave is done with buffer (s-1) % RB), issue B(s+RB-1)
-    // into that buffer, and start reading stage s+1.  After the last MFMA,
-    // refill A with A(s+RA).  Loads past the last stage re-read the last
-    // stage.
+    // stage s (A in A, B in LDS buffer s % 4).  Loads past the last stage
+    // re-read the last stage into buffers and registers no stage reads.
     auto stage = [&](int s, u32x4_t (&A)[A_FRAGS]) {
         const uint8_t* bcur = lds + (s % kRingB) * B_STAGE_BYTES;
         const uint8_t* bnext = lds + ((s + 1) % kRingB) * B_STAGE_BYTES;
+        const int sb = min(s + 2, n_stages - 1), bbuf = (s + 2) % kRingB;
+        const int sa = min(s + kRingA, n_stages - 1);
 #pragma unroll
         for (int u = 0; u < kUnits; ++u) {
-            if (u == kUnits - kLook) {
-                wait_and_barrier();
-                load_b(min(s + kRingB - 1, n_stages - 1), (s + kRingB - 1) % kRingB);
-            }
+            if (u == kBarrierUnit) wait_and_barrier();
+            if (u % 4 == 1) load_b1(sb, bbuf, u / 4);
+#pragma unroll
+            for (int fb = 0; fb < FB; ++fb)
+#pragma unroll
+                for (int j = 0; j < KS; ++j)
+                    if (a_load_unit(fb, j) == u) load_a1(sa, fb, j, A[fb * KS + j]);
             if (u + kLook < kUnits)
                 read_unit(bcur, u + kLook);
             else
@@ -181,24 +214,31 @@ __device__ __forceinline__ void tile_loop(const TileCtx& c, int n_pairs, uint8_t
             }
             __builtin_amdgcn_sched_barrier(0);
         }
-        load_a(min(s + kRingA, n_stages - 1), A);
+#pragma unroll
+        for (int fb = 0; fb < FB; ++fb)
+#pragma unroll
+            for (int j = 0; j < KS; ++j)
+                if (a_load_unit(fb, j) == kUnits) load_a1(sa, fb, j, A[fb * KS + j]);
     };
 
-    // prologue: B stages 0..RB-2 and A stages 0..RA-1 in flight; wait for
-    // them, then read the first kLook units of stage 0 (the loads of every
-    // stage run in order: stage 0 publishes B(1) and issues B(RB-1))
-    static_assert(kRingB - 1 >= kRingA - 1, "prologue issues B ahead of A");
+    // prologue: B(0), B(1) and A(0..2); wait for them, then read the first
+    // kLook units of stage 0
 #pragma unroll
-    for (int i = 0; i < kRingB - 1; ++i) {
-        load_b(min(i, n_stages - 1), i);
-        if (i < kRingA) load_a(min(i, n_stages - 1), ra[i]);
-    }
+    for (int i = 0; i < 2; ++i)
+#pragma unroll
+        for (int q = 0; q < B_LOADS; ++q) load_b1(min(i, n_stages - 1), i, q);
+#pragma unroll
+    for (int i = 0; i < kRingA; ++i)
+#pragma unroll
+        for (int fb = 0; fb < FB; ++fb)
+#pragma unroll
+            for (int j = 0; j < KS; ++j) load_a1(min(i, n_stages - 1), fb, j, ra[i][fb * KS + j]);
     __builtin_amdgcn_s_waitcnt(kWaitAll);
     __builtin_amdgcn_s_barrier();
     asm volatile("" ::: "memory");
 #pragma unroll
     for (int u = 0; u < kLook; ++u) read_unit(lds, u);
-    // RA stages per iteration, so that the A ring is indexed statically
+    // three stages per iteration, so that the A ring is indexed statically
     int s = 0;
     for (; s + kRingA <= n_stages; s += kRingA) {
         stage(s + 0, ra[0]);
