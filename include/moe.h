@@ -80,6 +80,8 @@ typedef enum {
  *   n_layers         : layers held in the arena (>= 1).
  *   max_tokens       : largest T any call will pass; sizes the workspace.
  *                      max_tokens * d_model * 2 must stay below 2^31.
+ *   d_model * ffn_dim * 4 (one expert's packed gate/up bytes) must stay
+ *                      below 2^31.
  *   flags            : must be 0. */
 typedef struct {
     int32_t d_model, ffn_dim, n_experts, top_k;

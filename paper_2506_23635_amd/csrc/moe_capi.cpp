@@ -49,6 +49,8 @@ const char* check_config(const moe_config* c)
     if (c->max_tokens < 1 || c->max_tokens > (1 << 20)) return "max_tokens must be in [1, 2^20]";
     if ((int64_t)c->max_tokens * c->d_model * 2 > INT32_MAX)
         return "max_tokens * d_model * 2 must stay below 2^31 (32-bit gather offsets)";
+    if ((int64_t)c->d_model * c->ffn_dim * 4 > INT32_MAX)
+        return "d_model * ffn_dim * 4 (one expert's gate/up slab) must stay below 2^31";
     if (c->flags != 0) return "flags must be 0";
     return nullptr;
 }

@@ -51,6 +51,10 @@ constexpr int B_FRAGS = TB * KS;                  // 32 B fragments per stage
 constexpr int B_LOADS = B_FRAGS * 64 / kThreads;  // 8 per thread
 constexpr int B_STAGE_BYTES = B_FRAGS * kTileBytes;  // 32 KiB
 constexpr int kXcds = 8;
+#ifndef MOE_FT_BLOCK
+#define MOE_FT_BLOCK 1
+#endif
+constexpr int kFtBlock = MOE_FT_BLOCK;   // feature tiles per block of the tile order
 constexpr int kBufferFlags = 0x00020000;   // buffer descriptor word 3 (raw dword data, gfx9 family)
 constexpr int kWaitAll = (0x7 << 4) | (0xF << 8);   // vmcnt 0
 static_assert(kRingA == 3, "the K loop is unrolled by three stages");
@@ -81,8 +85,8 @@ __device__ __forceinline__ int b_swizzle(int R)
 }
 
 struct TileCtx {
-    const uint8_t* a_src;      // this lane's A bytes for feature block 0, stage 0, step 0
-    uint64_t a_fstride;        // bytes between 32-feature blocks (two row tiles)
+    __amdgpu_buffer_rsrc_t a_rsrc;  // buffer over the expert's packed slab (GU or DN)
+    uint32_t a_off[FB];        // this lane's A byte offset per feature block (stage 0, step 0)
     __amdgpu_buffer_rsrc_t b_rsrc;  // buffer over x (gate/up) or over the tile's rows of H
     uint32_t b_off[B_LOADS];   // byte offsets in b_rsrc of this lane's 16-byte chunk, per load
     uint32_t rd_off[KS];       // LDS byte offsets of this lane's B fragment piece, per K step
@@ -154,9 +158,9 @@ __device__ __forceinline__ void tile_loop(const TileCtx& c, int n_pairs, uint8_t
     // A fragment (fb, j) of stage s: K step j lives in K tile 2s + j/2,
     // second half of the tile for odd j (512 bytes on)
     auto load_a1 = [&](int s, int fb, int j, u32x4_t& dst) {
-        dst = *reinterpret_cast<const u32x4_t*>(c.a_src + fb * c.a_fstride +
-                                                (uint64_t)(2 * s + j / 2) * kTileBytes +
-                                                (j % 2) * (kTileBytes / 2));
+        dst = __builtin_bit_cast(u32x4_t, __builtin_amdgcn_raw_buffer_load_b128(
+                                              c.a_rsrc, c.a_off[fb] + (j / 2) * kTileBytes + (j % 2) * (kTileBytes / 2),
+                                              (uint32_t)s * (2 * kTileBytes), 0));
     };
     // B goes global -> LDS directly through buffer loads: a stage of B is
     // 256 rows x 128 bytes (64 K), row-major in LDS with the eight 16-byte
@@ -273,7 +277,7 @@ __device__ __forceinline__ void process_tile(const GemmArgs& a, int ft, int tt, 
     TileCtx c;
     c.n_stages = K / BK;
     c.lane = threadIdx.x & 63;
-    c.w = threadIdx.x >> 6;
+    c.w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);   // wave-uniform, in an SGPR
     const int lane = c.lane, w = c.w;
     // a wave past M (partial last feature tile) recomputes the last valid
     // slab, keeping every load unconditional, and skips its stores
@@ -281,10 +285,16 @@ __device__ __forceinline__ void process_tile(const GemmArgs& a, int ft, int tt, 
     const uint64_t rt0 =
         wave_on ? (uint64_t)ft * (BM / 16) + w * kWaveRt : (uint64_t)(M / 16 - kWaveRt);
     // A: lane l of a 32 x 16 fragment reads row l%32 of the block (row tile
-    // rt0 + 2 fb + (l%32)/16, granule row l%16) at K group l/32 of the step
-    c.a_src = wbase + tile_offset(rt0 + ((lane & 31) >> 4), 0, KT) +
-              (((lane >> 5) * 16) + (lane & 15)) * 16;
-    c.a_fstride = 2 * KT * kTileBytes;
+    // rt0 + 2 fb + (l%32)/16, granule row l%16) at K group l/32 of the step.
+    // Buffer loads over the expert's slab (the library caps a slab below
+    // 2^31 bytes, so offsets fit 32 bits; the size bounds every load).
+    const uint64_t slab_bytes = kMode == kGateUp ? a.gu_bytes : a.expert_bytes - a.gu_bytes;
+    c.a_rsrc = __builtin_amdgcn_make_buffer_rsrc(const_cast<uint8_t*>(wbase), 0, (int)slab_bytes,
+                                                 kBufferFlags);
+#pragma unroll
+    for (int fb = 0; fb < FB; ++fb)
+        c.a_off[fb] = (uint32_t)tile_offset(rt0 + 2 * fb + ((lane & 31) >> 4), 0, KT) +
+                      (uint32_t)(((lane >> 5) * 16) + (lane & 15)) * 16;
     // B: a stage holds, for each of the 256 token rows R of the tile, the
     // 128 bytes of K [64 s, 64 s + 64) as eight 16-byte chunks; chunk c sits
     // in slot c ^ swz(R) so that the MFMA reads (8 consecutive rows at one
@@ -376,12 +386,16 @@ __global__ __launch_bounds__(kThreads) void gemm_kernel(GemmArgs a)
     const int M = kMode == kGateUp ? 2 * a.f : a.d;
     const int n_ftiles = (M + BM - 1) / BM;
     // XCD-aware numbering: hardware hands block b to XCD b % 8; give each XCD
-    // a contiguous run of logical tiles (token tile fastest, so the tiles
-    // that share a weight slab run together on one XCD).
+    // a contiguous run of logical tiles.  Logical tiles walk blocks of
+    // kFtBlock feature tiles: within a block, feature tile fastest, then
+    // token tile, so the workgroups running together on one XCD share both
+    // token tiles (B) and the weight slabs of their experts (A) in its L2.
     const int per_xcd = gridDim.x / kXcds;
     const int logical = (blockIdx.x % kXcds) * per_xcd + blockIdx.x / kXcds;
-    const int ft = logical / a.max_tiles;
-    const int tt = logical % a.max_tiles;
+    const int blk = logical / (a.max_tiles * kFtBlock);
+    const int rem = logical % (a.max_tiles * kFtBlock);
+    const int tt = rem / kFtBlock;
+    const int ft = blk * kFtBlock + rem % kFtBlock;
     if (ft >= n_ftiles || tt >= *a.n_tiles) return;
     process_tile<kMode>(a, ft, tt, lds);
 }
@@ -394,7 +408,8 @@ template <int kMode>
 static hipError_t launch_gemm(const moe::GemmArgs* a, hipStream_t s)
 {
     const int M = kMode == moe::kGateUp ? 2 * a->f : a->d;
-    const int n = (M + moe::BM - 1) / moe::BM * a->max_tiles;
+    const int n_blocks = ((M + moe::BM - 1) / moe::BM + moe::kFtBlock - 1) / moe::kFtBlock;
+    const int n = n_blocks * moe::kFtBlock * a->max_tiles;
     const int grid = (n + moe::kXcds - 1) / moe::kXcds * moe::kXcds;
     hipLaunchKernelGGL((moe::gemm_kernel<kMode>), dim3(grid), dim3(moe::kThreads), 0, s, *a);
     return hipGetLastError();

@@ -60,9 +60,10 @@ def test_weight_bytes_formula():
                                  dict(n_experts=0), dict(n_experts=65), dict(top_k=0),
                                  dict(top_k=17), dict(expert_begin=13, n_local_experts=4),
                                  dict(n_layers=0), dict(max_tokens=0), dict(flags=1),
-                                 dict(max_tokens=174763)])
+                                 dict(max_tokens=174763), dict(ffn_dim=87424)])
 def test_bad_configs_rejected(bad):
-    # max_tokens 174763: x is then 2^31 bytes or more, past the GEMM's 32-bit gather offsets
+    # max_tokens 174763: x is then 2^31 bytes or more, past the GEMM's 32-bit gather offsets;
+    # ffn_dim 87424: one expert's gate/up slab (4 * d * f bytes) is 2^31 bytes or more
     cfg = dbrx(**bad)
     if bad.get("n_experts") == 0:
         cfg.n_local_experts = 0
