@@ -192,17 +192,11 @@ moe_status do_route(moe_ctx* ctx, int layer, const uint16_t* x, int T, const flo
                                            &ctx->rv, s);
         });
         if (e != hipSuccess) return hip_fail(ctx, e, "route kernel launch");
-    } else if (!logits_in && T <= moe_route_small_max_tokens()) {
-        e = timed(ctx, MOE_K_ROUTE, s, [&] {
-            return moe_launch_route_small(x, wrT, bias, T, c.d_model, c.n_experts, c.top_k,
-                                          c.expert_begin, c.n_local_experts, tile_rows, &ctx->rv, s);
-        });
-        if (e != hipSuccess) return hip_fail(ctx, e, "route kernel launch");
     } else {
         if (!logits_in) {
             e = timed(ctx, MOE_K_ROUTER, s, [&] {
-                return moe_launch_router_logits(x, wrT, bias, T, c.d_model, c.n_experts,
-                                                ctx->rv.logits, s);
+                return moe_launch_router_select(x, wrT, bias, T, c.d_model, c.n_experts,
+                                                c.top_k, &ctx->rv, s);
             });
             if (e != hipSuccess) return hip_fail(ctx, e, "router kernel launch");
         }

@@ -149,7 +149,6 @@ struct GemmArgs {
 extern "C" {
 hipError_t moe_launch_pack(const uint16_t* src, int K, int N, void* dst, int rt_mul, int rt_add,
                            hipStream_t s);
-int moe_route_small_max_tokens();
 int moe_route_decode_ok(int T, int E, int k);
 int moe_route_decode_wgs(int d);
 hipError_t moe_launch_zero_counter(unsigned int* counter, hipStream_t s);
@@ -157,11 +156,8 @@ hipError_t moe_launch_route_decode(const uint16_t* x, const float* wrT, const fl
                                    double* partial, unsigned int* counter, int T, int d, int E,
                                    int k, int e_begin, int n_local, int tile_rows,
                                    const moe::RouteView* rv, hipStream_t s);
-hipError_t moe_launch_route_small(const uint16_t* x, const float* wrT, const float* bias, int T,
-                                  int d, int E, int k, int e_begin, int n_local, int tile_rows,
-                                  const moe::RouteView* rv, hipStream_t s);
-hipError_t moe_launch_router_logits(const uint16_t* x, const float* wrT, const float* bias, int T,
-                                    int d, int E, float* logits, hipStream_t s);
+hipError_t moe_launch_router_select(const uint16_t* x, const float* wrT, const float* bias, int T,
+                                   int d, int E, int k, const moe::RouteView* rv, hipStream_t s);
 hipError_t moe_launch_route(const float* logits_in, int T, int E, int k, int e_begin, int n_local,
                             int tile_rows, const moe::RouteView* rv, hipStream_t s);
 hipError_t moe_launch_transpose_router(const float* wr, int d, int E, float* wrT, hipStream_t s);

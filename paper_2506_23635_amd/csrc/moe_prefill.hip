@@ -152,7 +152,7 @@ __device__ __forceinline__ void tile_loop(const TileCtx& c, int n_pairs, uint8_t
                                           f32x16_t (&acc)[FB][TB])
 {
     const int n_stages = c.n_stages;
-    const int w = c.w, lane = c.lane;
+    const int w = c.w;
     u32x4_t ra[kRingA][A_FRAGS];
     u32x4_t bw[kWin];
     // A fragment (fb, j) of stage s: K step j lives in K tile 2s + j/2,

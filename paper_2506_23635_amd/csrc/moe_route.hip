@@ -10,21 +10,19 @@
 // that every load is 16 bytes.
 //
 // Kernels
-//   route_small_kernel  (T <= kSmallT): one 1024-thread workgroup computes the
-//       logits (thread = expert x d-slice, fixed-order LDS reduction), then
-//       selects, weighs and permutes -- a single launch for a decode step.
-//   router_logits_kernel (larger T): 4 tokens per 256-thread workgroup, each
-//       (token, expert) dot product split over four threads and summed in
-//       fixed order through LDS.
+//   router_select_kernel: 8 tokens per workgroup, a wave takes 4 tokens x 8
+//       experts, each dot product split over the 64 lanes and summed by a
+//       fixed butterfly; then each token's selection.
 //   route_decode_kernel (T <= 16, E <= 16, T*k <= 64): the logits spread over
 //       d/512 workgroups, the last one to finish selects and permutes.
-//   route_kernel: selection, weights and permutation from fp32 logits.
+//   select_kernel: selection and weights from caller-supplied fp32 logits.
+//   permute_kernel: the permutation and the GEMM tile list (one workgroup).
 //
 // Selection: the k largest logits, ties to the lower expert id, slots ordered
 // by (logit desc, id asc); weights = softmax over the selected logits (fp32).
-// Permutation: block-wide prefix sums per local expert over pairs in (token,
-// slot) order, which gives rows grouped by expert, then token -- no atomics,
-// so the order is deterministic.
+// Permutation: prefix sums per local expert over pairs in (token, slot)
+// order, which gives rows grouped by expert, then token -- no atomic decides
+// a row, so the order is deterministic.
 #include <algorithm>
 
 #include "moe_common.h"
@@ -33,19 +31,6 @@ namespace moe {
 
 constexpr int kRouteThreads = 1024;
 constexpr int kRouteWaves = kRouteThreads / kWave;
-constexpr int kSmallPartials = 4096;   // doubles of LDS for the slice partials
-
-struct RouteArgs {
-    const uint16_t* x;        // [T, d]          (route_small_kernel)
-    const float* wrT;         // [E, d]          (route_small_kernel)
-    const float* logits_in;   // [T, E] or null  (route_kernel: read from here if set)
-    const float* bias;        // [E] or null     (route_small_kernel)
-    int T, d, E, k;
-    int e_begin, n_local;
-    int tile_rows;            // token rows per GEMM tile
-    RouteView rv;
-};
-
 // Selection and weights for token t from logits l[0..E) (any address space).
 // The logits, the chosen ids and their exponentials stay in registers
 // (kMaxE and kMaxK bound the static arrays; E <= 64 always).
@@ -96,130 +81,6 @@ __device__ inline void select_token_any(const float* l, int t, int E, int k, con
     else select_token<64>(l, t, E, k, rv);
 }
 
-// Expert-grouped permutation of the T*k pairs (whole workgroup); needs the
-// workgroup's topk_idx writes to be visible (caller syncs).  Each thread owns
-// a contiguous chunk of pairs; per group of 16 experts, every thread counts
-// its pairs per expert, a wave-level inclusive scan and one LDS pass over the
-// wave totals give each thread its first row per expert, and the thread then
-// writes its rows -- three barriers per expert group.
-constexpr int kPermExperts = 16;
-constexpr int kPermMaxChunk = 8;
-
-__device__ void build_permutation(const RouteArgs& a, int (*lds_tot)[kPermExperts],
-                                  int* lds_counts)
-{
-    const int T = a.T, E = a.E, k = a.k;
-    const int tid = threadIdx.x;
-    const int lane = tid & 63;
-    const int wid = tid >> 6;
-    const RouteView& rv = a.rv;
-    const int P = T * k;
-    const int chunk = (P + kRouteThreads - 1) / kRouteThreads;
-    const int p0 = min(P, tid * chunk);
-    const int p1 = min(P, p0 + chunk);
-    const int lo = a.e_begin, hi = a.e_begin + a.n_local;
-    // the chunk's expert ids, held in registers when the chunk is short
-    int ids[kPermMaxChunk];
-    const bool in_regs = chunk <= kPermMaxChunk;
-#pragma unroll
-    for (int q = 0; q < kPermMaxChunk; ++q)
-        ids[q] = (in_regs && p0 + q < p1) ? rv.topk_idx[p0 + q] : -1;
-    auto id_at = [&](int p) {
-        if (in_regs) {
-            int v = -1;
-#pragma unroll
-            for (int q = 0; q < kPermMaxChunk; ++q)
-                if (p - p0 == q) v = ids[q];
-            return v;
-        }
-        return rv.topk_idx[p];
-    };
-    for (int p = p0; p < p1; ++p) {
-        const int e = id_at(p);
-        if (e < lo || e >= hi) rv.pair_row[p] = -1;
-    }
-    int running = 0;   // rows of all earlier experts
-    for (int e0 = 0; e0 < E; e0 += kPermExperts) {
-        int cnt[kPermExperts];
-#pragma unroll
-        for (int j = 0; j < kPermExperts; ++j) cnt[j] = 0;
-        for (int p = p0; p < p1; ++p) {
-            const int e = id_at(p);
-#pragma unroll
-            for (int j = 0; j < kPermExperts; ++j) cnt[j] += (e == e0 + j) ? 1 : 0;
-        }
-        // wave-level inclusive scans of the 16 counters
-        int inc[kPermExperts];
-#pragma unroll
-        for (int j = 0; j < kPermExperts; ++j) {
-            int v = cnt[j];
-#pragma unroll
-            for (int off = 1; off < 64; off <<= 1) {
-                const int o = __shfl_up(v, off, 64);
-                if (lane >= off) v += o;
-            }
-            inc[j] = v;
-        }
-        if (lane == 63) {
-#pragma unroll
-            for (int j = 0; j < kPermExperts; ++j) lds_tot[wid][j] = inc[j];
-        }
-        __syncthreads();
-        int base[kPermExperts];
-        int run = running;
-#pragma unroll
-        for (int j = 0; j < kPermExperts; ++j) {
-            const int e = e0 + j;
-            int before = 0, tot = 0;
-            for (int w = 0; w < kRouteWaves; ++w) {
-                const int c = lds_tot[w][j];
-                before += (w < wid) ? c : 0;
-                tot += c;
-            }
-            const bool local = e < E && e >= lo && e < hi;
-            if (!local) tot = 0;
-            base[j] = run + before + inc[j] - cnt[j];
-            if (tid == 0 && e < E) {
-                rv.counts[e] = tot;
-                rv.offsets[e] = run;
-                lds_counts[e] = tot;
-            }
-            run += tot;
-        }
-        for (int p = p0; p < p1; ++p) {
-            const int e = id_at(p);
-            if (e >= e0 && e < e0 + kPermExperts && e >= lo && e < hi) {
-                int r = 0;
-#pragma unroll
-                for (int j = 0; j < kPermExperts; ++j)
-                    if (e == e0 + j) r = base[j]++;
-                rv.pair_row[p] = r;
-                rv.row_token[r] = p / k;
-            }
-        }
-        running = run;
-        __syncthreads();
-    }
-    if (tid == 0) {
-        rv.offsets[E] = running;
-        int na = 0, nt = 0, row = 0;
-        for (int e = 0; e < E; ++e) {
-            const int c = lds_counts[e];
-            if (c > 0) {
-                rv.active[1 + na++] = e;
-                for (int r = 0; r < c; r += a.tile_rows) {
-                    rv.tiles[2 * nt] = e;
-                    rv.tiles[2 * nt + 1] = row + r;
-                    ++nt;
-                }
-            }
-            row += c;
-        }
-        rv.active[0] = na;
-        *rv.n_tiles = nt;
-    }
-}
-
 __device__ inline void fma8(double& acc, const u32x4_t xv, const float4 w0, const float4 w1)
 {
     acc = fma((double)__uint_as_float(xv[0] << 16), (double)w0.x, acc);
@@ -233,61 +94,6 @@ __device__ inline void fma8(double& acc, const u32x4_t xv, const float4 w0, cons
 }
 
 constexpr int kSmallT = 16;
-
-__global__ __launch_bounds__(kRouteThreads) void route_small_kernel(RouteArgs a)
-{
-    __shared__ double part[kSmallPartials];
-    __shared__ float lg[kSmallT * 64];
-    __shared__ int lds_tot[kRouteWaves][kPermExperts];
-    __shared__ int lds_counts[64];
-    const int T = a.T, E = a.E, d = a.d;
-    const int tid = threadIdx.x;
-
-    // slices: S slices of the d axis per expert, S*T*E partials fit in LDS
-    int S = kRouteThreads / E;
-    while (S > 1 && S * T * E > kSmallPartials) S >>= 1;
-    const int groups = d / 8;                         // 8-element groups
-    const int per = (groups + S - 1) / S;             // groups per slice
-    if (tid < E * S) {
-        const int e = tid % E;
-        const int s = tid / E;
-        const int g0 = s * per;
-        const int g1 = min(groups, g0 + per);
-        double acc[kSmallT];
-#pragma unroll
-        for (int t = 0; t < kSmallT; ++t) acc[t] = 0.0;
-        const float* wrow = a.wrT + (int64_t)e * d;
-#pragma unroll 6
-        for (int g = g0; g < g1; ++g) {
-            const float4 w0 = *reinterpret_cast<const float4*>(wrow + g * 8);
-            const float4 w1 = *reinterpret_cast<const float4*>(wrow + g * 8 + 4);
-#pragma unroll
-            for (int t = 0; t < kSmallT; ++t) {
-                if (t < T) {
-                    const u32x4_t xv = *reinterpret_cast<const u32x4_t*>(a.x + (int64_t)t * d + g * 8);
-                    fma8(acc[t], xv, w0, w1);
-                }
-            }
-        }
-#pragma unroll
-        for (int t = 0; t < kSmallT; ++t)
-            if (t < T) part[(s * T + t) * E + e] = acc[t];
-    }
-    __syncthreads();
-    if (tid < T * E) {
-        const int t = tid / E, e = tid % E;
-        double sum = 0.0;
-        for (int s = 0; s < S; ++s) sum += part[(s * T + t) * E + e];
-        float v = (float)sum;
-        if (a.bias) v = __fadd_rn(v, a.bias[e]);
-        lg[t * 64 + e] = v;
-        a.rv.logits[(int64_t)t * E + e] = v;
-    }
-    __syncthreads();
-    if (tid < T) select_token_any(&lg[tid * 64], tid, E, a.k, a.rv);
-    __syncthreads();
-    build_permutation(a, lds_tot, lds_counts);
-}
 
 // Decode routing (T <= 16, E <= 16, T*k <= 64): the logits are spread over
 // n_wg workgroups, each owning d/n_wg of the reduction axis (one 8-wide group
@@ -424,71 +230,190 @@ __global__ __launch_bounds__(kRouteThreads) void route_decode_kernel(DecodeRoute
 
 __global__ void zero_u32_kernel(unsigned int* p) { *p = 0u; }
 
-// logits for 4 tokens per workgroup: thread = (d-split tid/64, token
-// (tid/16)%4, expert slot tid%16) over experts slot, slot+16, ...; each thread
-// streams a quarter of the token row and of the expert row in 16-byte vectors
-// with two interleaved accumulators, and the four quarter sums are added in
-// split order through LDS.
-constexpr int kLogitTok = 4;
-constexpr int kLogitSplit = 4;
+// Router and selection for many tokens: 8 tokens per 256-thread workgroup;
+// wave w takes tokens 4(w/2) .. +3 and experts 8(w%2) .. +7 (then +16, ...).
+// Lane l accumulates, in fp64, the 8-element groups l, l + 64, ... of the
+// reduction axis for its 4 tokens x 8 experts, so each router value it
+// loads serves 4 tokens and each x value 8 experts, and a wave reads 512
+// consecutive elements of every row per step.  A fixed xor butterfly over
+// the 64 lanes sums the lane partials; lane 0's sums are rounded once to
+// fp32 and the bias added in fp32; then one thread per token selects its
+// experts from the logits in LDS.
+constexpr int kRsTokWave = 4;
+constexpr int kRsExp = 8;
+constexpr int kRsTok = 2 * kRsTokWave;
+constexpr int kRsThreads = 4 * kWave;
 
-__global__ __launch_bounds__(256) void router_logits_kernel(const uint16_t* __restrict__ x,
-                                                            const float* __restrict__ wrT,
-                                                            const float* __restrict__ bias, int T,
-                                                            int d, int E,
-                                                            float* __restrict__ logits)
+__global__ __launch_bounds__(kRsThreads) void router_select_kernel(const uint16_t* __restrict__ x,
+                                                                   const float* __restrict__ wrT,
+                                                                   const float* __restrict__ bias,
+                                                                   int T, int d, int E, int k,
+                                                                   RouteView rv)
 {
-    __shared__ double part[kLogitSplit][kLogitTok][64];
-    const int tid = threadIdx.x;
-    const int sp = tid >> 6;
-    const int tl = (tid >> 4) & 3;
-    const int es = tid & 15;
-    const int t = blockIdx.x * kLogitTok + tl;
-    const int q = d / kLogitSplit;            // d is a multiple of 256
-    if (t < T) {
-        const uint16_t* xr = x + (int64_t)t * d + sp * q;
-        for (int e = es; e < E; e += 16) {
-            const float* wr = wrT + (int64_t)e * d + sp * q;
-            double a0 = 0.0, a1 = 0.0;
-#pragma unroll 8
-            for (int g = 0; g < q; g += 16) {
-                const u32x4_t x0 = *reinterpret_cast<const u32x4_t*>(xr + g);
-                const u32x4_t x1 = *reinterpret_cast<const u32x4_t*>(xr + g + 8);
-                const float4 w0 = *reinterpret_cast<const float4*>(wr + g);
-                const float4 w1 = *reinterpret_cast<const float4*>(wr + g + 4);
-                const float4 w2 = *reinterpret_cast<const float4*>(wr + g + 8);
-                const float4 w3 = *reinterpret_cast<const float4*>(wr + g + 12);
-                fma8(a0, x0, w0, w1);
-                fma8(a1, x1, w2, w3);
+    __shared__ float lg[kRsTok][64];
+    const int wid = threadIdx.x / kWave, lane = threadIdx.x % kWave;
+    const int tg = wid / 2, eh = wid % 2;
+    const int t0 = blockIdx.x * kRsTok + tg * kRsTokWave;
+    for (int e0 = eh * kRsExp; e0 < E; e0 += 2 * kRsExp) {
+        double acc[kRsTokWave][kRsExp];
+#pragma unroll
+        for (int i = 0; i < kRsTokWave; ++i)
+#pragma unroll
+            for (int j = 0; j < kRsExp; ++j) acc[i][j] = 0.0;
+        // tokens past T and experts past E (partial last groups) recompute
+        // token T-1 / expert E-1 so that the loop has no branch; their sums
+        // are dropped
+        const uint16_t* xr[kRsTokWave];
+        const float* wr[kRsExp];
+#pragma unroll
+        for (int i = 0; i < kRsTokWave; ++i) xr[i] = x + (int64_t)min(t0 + i, T - 1) * d;
+#pragma unroll
+        for (int j = 0; j < kRsExp; ++j) wr[j] = wrT + (int64_t)min(e0 + j, E - 1) * d;
+        for (int g = lane * 8; g < d; g += kWave * 8) {
+            u32x4_t xv[kRsTokWave];
+#pragma unroll
+            for (int i = 0; i < kRsTokWave; ++i) xv[i] = *reinterpret_cast<const u32x4_t*>(xr[i] + g);
+#pragma unroll
+            for (int j = 0; j < kRsExp; ++j) {
+                const float4 w0 = *reinterpret_cast<const float4*>(wr[j] + g);
+                const float4 w1 = *reinterpret_cast<const float4*>(wr[j] + g + 4);
+#pragma unroll
+                for (int i = 0; i < kRsTokWave; ++i) fma8(acc[i][j], xv[i], w0, w1);
             }
-            part[sp][tl][e] = a0 + a1;
+        }
+#pragma unroll
+        for (int i = 0; i < kRsTokWave; ++i)
+#pragma unroll
+            for (int j = 0; j < kRsExp; ++j)
+#pragma unroll
+                for (int off = kWave / 2; off >= 1; off >>= 1)
+                    acc[i][j] += __shfl_xor(acc[i][j], off, kWave);
+        if (lane == 0) {
+#pragma unroll
+            for (int i = 0; i < kRsTokWave; ++i)
+#pragma unroll
+                for (int j = 0; j < kRsExp; ++j) {
+                    const int t = t0 + i, e = e0 + j;
+                    if (t < T && e < E) {
+                        float v = (float)acc[i][j];
+                        if (bias) v = __fadd_rn(v, bias[e]);
+                        lg[tg * kRsTokWave + i][e] = v;
+                        rv.logits[(int64_t)t * E + e] = v;
+                    }
+                }
         }
     }
     __syncthreads();
-    if (sp == 0 && t < T) {
-        for (int e = es; e < E; e += 16) {
-            double s = part[0][tl][e];
-            for (int k = 1; k < kLogitSplit; ++k) s += part[k][tl][e];
-            float v = (float)s;
-            if (bias) v = __fadd_rn(v, bias[e]);
-            logits[(int64_t)t * E + e] = v;
-        }
+    if (threadIdx.x < kRsTok) {
+        const int t = blockIdx.x * kRsTok + threadIdx.x;
+        if (t < T) select_token_any(&lg[threadIdx.x][0], t, E, k, rv);
     }
 }
 
-__global__ __launch_bounds__(kRouteThreads) void route_kernel(RouteArgs a)
+// Selection from caller-supplied fp32 logits (copied into the routing
+// view): one thread per token.
+__global__ __launch_bounds__(256) void select_kernel(const float* __restrict__ logits_in, int T,
+                                                     int E, int k, RouteView rv)
 {
-    __shared__ int lds_tot[kRouteWaves][kPermExperts];
-    __shared__ int lds_counts[64];
-    const float* src = a.logits_in ? a.logits_in : a.rv.logits;
-    for (int t = threadIdx.x; t < a.T; t += kRouteThreads) {
-        if (a.logits_in)
-            for (int e = 0; e < a.E; ++e)
-                a.rv.logits[(int64_t)t * a.E + e] = src[(int64_t)t * a.E + e];
-        select_token_any(src + (int64_t)t * a.E, t, a.E, a.k, a.rv);
+    const int t = blockIdx.x * blockDim.x + threadIdx.x;
+    if (t >= T) return;
+    const float* l = logits_in + (int64_t)t * E;
+    for (int e = 0; e < E; ++e) rv.logits[(int64_t)t * E + e] = l[e];
+    select_token_any(l, t, E, k, rv);
+}
+
+// Expert-grouped permutation of the T*k pairs (one 1024-thread workgroup),
+// rows grouped by local expert, then by pair (token, slot) order.
+//  1. counts: LDS histogram of the local pairs (order-free); thread 0 then
+//     writes counts, offsets, the active-expert list and the GEMM tile list.
+//  2. rows: pairs in rounds of 1024 x 8; each thread holds 8 consecutive
+//     pairs; per local expert, a wave scan of the per-thread counts plus the
+//     wave totals (LDS) give each pair its row after the expert's cursor.
+// Deterministic: no atomic decides a row.
+constexpr int kPermChunk = 8;
+
+struct PermArgs {
+    int T, E, k, e_begin, n_local, tile_rows;
+    RouteView rv;
+};
+
+__global__ __launch_bounds__(kRouteThreads) void permute_kernel(PermArgs a)
+{
+    __shared__ int hist[64];
+    __shared__ int cursor[64];
+    __shared__ int wtot[kRouteWaves];
+    const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
+    const int E = a.E, k = a.k, P = a.T * a.k;
+    const int lo = a.e_begin, hi = a.e_begin + a.n_local;
+    const RouteView& rv = a.rv;
+    if (tid < 64) hist[tid] = 0;
+    __syncthreads();
+    for (int p = tid; p < P; p += kRouteThreads) {
+        const int e = rv.topk_idx[p];
+        if (e >= lo && e < hi) atomicAdd(&hist[e], 1);
     }
     __syncthreads();
-    build_permutation(a, lds_tot, lds_counts);
+    if (tid == 0) {
+        int run = 0, na = 0, nt = 0;
+        for (int e = 0; e < E; ++e) {
+            const int c = hist[e];
+            rv.counts[e] = c;
+            rv.offsets[e] = run;
+            cursor[e] = run;
+            if (c > 0) {
+                rv.active[1 + na++] = e;
+                for (int r = 0; r < c; r += a.tile_rows) {
+                    rv.tiles[2 * nt] = e;
+                    rv.tiles[2 * nt + 1] = run + r;
+                    ++nt;
+                }
+            }
+            run += c;
+        }
+        rv.offsets[E] = run;
+        rv.active[0] = na;
+        *rv.n_tiles = nt;
+    }
+    __syncthreads();
+    for (int r0 = 0; r0 < P; r0 += kRouteThreads * kPermChunk) {
+        const int p0 = r0 + tid * kPermChunk;
+        int ids[kPermChunk];
+#pragma unroll
+        for (int q = 0; q < kPermChunk; ++q) {
+            ids[q] = p0 + q < P ? rv.topk_idx[p0 + q] : -1;
+            if (p0 + q < P && (ids[q] < lo || ids[q] >= hi)) rv.pair_row[p0 + q] = -1;
+        }
+        for (int e = lo; e < hi; ++e) {
+            int cnt = 0;
+#pragma unroll
+            for (int q = 0; q < kPermChunk; ++q) cnt += ids[q] == e ? 1 : 0;
+            int inc = cnt;
+#pragma unroll
+            for (int off = 1; off < 64; off <<= 1) {
+                const int o = __shfl_up(inc, off, 64);
+                if (lane >= off) inc += o;
+            }
+            if (lane == 63) wtot[wid] = inc;
+            __syncthreads();
+            int before = 0, tot = 0;
+            for (int w = 0; w < kRouteWaves; ++w) {
+                const int c = wtot[w];
+                before += w < wid ? c : 0;
+                tot += c;
+            }
+            int row = cursor[e] + before + inc - cnt;
+#pragma unroll
+            for (int q = 0; q < kPermChunk; ++q) {
+                if (ids[q] == e) {
+                    rv.pair_row[p0 + q] = row;
+                    rv.row_token[row] = (p0 + q) / k;
+                    ++row;
+                }
+            }
+            __syncthreads();   // every thread has read wtot and cursor[e]
+            if (tid == 0) cursor[e] += tot;
+        }
+    }
 }
 
 // wrT[e][i] = wr[i][e]
@@ -504,22 +429,6 @@ __global__ __launch_bounds__(256) void transpose_router_kernel(const float* __re
 }
 
 }  // namespace moe
-
-extern "C" int moe_route_small_max_tokens() { return moe::kSmallT; }
-
-extern "C" hipError_t moe_launch_route_small(const uint16_t* x, const float* wrT,
-                                             const float* bias, int T, int d, int E, int k,
-                                             int e_begin, int n_local, int tile_rows,
-                                             const moe::RouteView* rv, hipStream_t s)
-{
-    moe::RouteArgs a{};
-    a.x = x; a.wrT = wrT; a.logits_in = nullptr; a.bias = bias;
-    a.T = T; a.d = d; a.E = E; a.k = k;
-    a.e_begin = e_begin; a.n_local = n_local; a.tile_rows = tile_rows;
-    a.rv = *rv;
-    hipLaunchKernelGGL(moe::route_small_kernel, dim3(1), dim3(moe::kRouteThreads), 0, s, a);
-    return hipGetLastError();
-}
 
 extern "C" int moe_route_decode_ok(int T, int E, int k)
 {
@@ -550,13 +459,13 @@ extern "C" hipError_t moe_launch_route_decode(const uint16_t* x, const float* wr
     return hipGetLastError();
 }
 
-extern "C" hipError_t moe_launch_router_logits(const uint16_t* x, const float* wrT,
-                                               const float* bias, int T, int d, int E,
-                                               float* logits, hipStream_t s)
+extern "C" hipError_t moe_launch_router_select(const uint16_t* x, const float* wrT,
+                                               const float* bias, int T, int d, int E, int k,
+                                               const moe::RouteView* rv, hipStream_t s)
 {
-    const int grid = (T + moe::kLogitTok - 1) / moe::kLogitTok;
-    hipLaunchKernelGGL(moe::router_logits_kernel, dim3(grid), dim3(256), 0, s, x, wrT, bias, T, d,
-                       E, logits);
+    const int grid = (T + moe::kRsTok - 1) / moe::kRsTok;
+    hipLaunchKernelGGL(moe::router_select_kernel, dim3(grid), dim3(moe::kRsThreads), 0, s, x, wrT,
+                       bias, T, d, E, k, *rv);
     return hipGetLastError();
 }
 
@@ -564,12 +473,17 @@ extern "C" hipError_t moe_launch_route(const float* logits_in, int T, int E, int
                                        int n_local, int tile_rows, const moe::RouteView* rv,
                                        hipStream_t s)
 {
-    moe::RouteArgs a{};
-    a.logits_in = logits_in;
+    if (logits_in) {
+        hipLaunchKernelGGL(moe::select_kernel, dim3((T + 255) / 256), dim3(256), 0, s, logits_in, T,
+                           E, k, *rv);
+        const hipError_t e = hipGetLastError();
+        if (e != hipSuccess) return e;
+    }
+    moe::PermArgs a{};
     a.T = T; a.E = E; a.k = k;
     a.e_begin = e_begin; a.n_local = n_local; a.tile_rows = tile_rows;
     a.rv = *rv;
-    hipLaunchKernelGGL(moe::route_kernel, dim3(1), dim3(moe::kRouteThreads), 0, s, a);
+    hipLaunchKernelGGL(moe::permute_kernel, dim3(1), dim3(moe::kRouteThreads), 0, s, a);
     return hipGetLastError();
 }
 

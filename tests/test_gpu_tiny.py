@@ -106,6 +106,42 @@ def test_route_from_x_matches_oracle(torch_mod, tiny_layer):
     _check_routing(got, idx, w, TINY.E)
 
 
+@pytest.mark.parametrize("T", [17, 300, 512])
+def test_route_from_x_many_tokens(torch_mod, tiny_layer, T):
+    """The multi-workgroup router + selection and the one-workgroup
+    permutation (every T above the decode routing's 16 tokens)."""
+    wl = TINY.with_(T=T)
+    x_t, x = x_device(wl)
+    got = tiny_layer.routing_tensors(tiny_layer.route(0, x_t))
+    lg = oracle.router_logits(x, wl.router())
+    assert np.all(np.abs(got["logits"] - lg) <= 1e-5 * np.abs(lg).max())
+    assert np.mean(got["logits"] == lg) >= 0.99
+    idx, w = oracle.route_from_logits(lg, wl.k)
+    _check_routing(got, idx, w, wl.E)
+
+
+# 24 experts, top-6: above the decode routing's limits (16 experts, 64 pairs),
+# so even one token goes through the general router and permutation
+WIDE = TINY.with_(E=24, k=6, T=40)
+
+
+@pytest.mark.parametrize("T", [1, 16, 40])
+def test_wide_routing_layer(torch_mod, T):
+    torch = torch_mod
+    wl = WIDE.with_(T=T)
+    layer = make_layer(wl, max_tokens=40)
+    load_workload_host(layer, wl)
+    x_t, x = x_device(wl)
+    got = layer.routing_tensors(layer.route(0, x_t))
+    ref = _oracle_full(wl, x)
+    lg = oracle.router_logits(x, wl.router())
+    assert np.all(np.abs(got["logits"] - lg) <= 1e-5 * np.abs(lg).max())
+    _check_routing(got, ref["idx"], ref["w"], wl.E)
+    y = _forward(torch, layer, x_t)
+    check_layer_output(y, ref["y64"])
+    layer.close()
+
+
 def _forward(torch, layer, x_t, T=None):
     T = x_t.shape[0] if T is None else T
     y = torch.empty((T, layer.cfg.d_model), dtype=torch.int16, device="cuda")
