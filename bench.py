@@ -86,6 +86,180 @@ def time_layer(layer, x, steps, warmup, kernel_events=True):
     return (t1 - t0) * 1e3 / steps, per_kernel, rt, dropped
 
 
+def graph_ms(fn, steps, warmup):
+    """Captures one call of fn in a HIP graph and times `steps` replays
+    (after `warmup` replays) with events; ms per replay."""
+    import torch
+    fn()
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        fn()
+    for _ in range(warmup):
+        g.replay()
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(steps):
+        g.replay()
+    e1.record()
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / steps
+    del g
+    return ms
+
+
+def load_layer_device(layer, wl, layer_idx, arena_layer, staging):
+    """Router and the context's local experts of layer `layer_idx` of `wl`,
+    generated on the device into `arena_layer` of the context."""
+    import torch
+    import moe_inputs as mi
+    s = layer.stream
+    d, f, E = wl.d, wl.f, wl.E
+    wr = torch.empty(d * E, dtype=torch.float32, device="cuda")
+    mi.gen_f32_device(wl.seed, mi.stream_id(mi.KIND_ROUTER, layer_idx), d * E, wl.sigma_r,
+                      wr.data_ptr(), s)
+    layer.load_router(arena_layer, wr, None)
+    g, u, dn = staging[: d * f], staging[d * f: 2 * d * f], staging[2 * d * f:]
+    c = layer.cfg
+    for e in range(c.expert_begin, c.expert_begin + c.n_local_experts):
+        mi.gen_bf16_device(wl.seed, mi.stream_id(mi.KIND_GATE, layer_idx, e), d * f, wl.sigma_w,
+                           g.data_ptr(), s)
+        mi.gen_bf16_device(wl.seed, mi.stream_id(mi.KIND_UP, layer_idx, e), d * f, wl.sigma_w,
+                           u.data_ptr(), s)
+        mi.gen_bf16_device(wl.seed, mi.stream_id(mi.KIND_DOWN, layer_idx, e), d * f, wl.sigma_w,
+                           dn.data_ptr(), s)
+        layer.load_expert(arena_layer, e, g, u, dn)
+
+
+def bf16_residual(x, y):
+    """bf16(x + y) for bf16 bit tensors (int16 views): the fp64 sum of two
+    bf16 values is exact and is rounded once, to 8 significant bits with ties
+    to even.  Used only to follow the chain for the traffic figure."""
+    import torch
+    v = x.view(torch.bfloat16).double() + y.view(torch.bfloat16).double()
+    m, ex = torch.frexp(v)
+    r = torch.ldexp(torch.round(m * 256.0), ex - 8)
+    return r.to(torch.bfloat16).view(torch.int16)
+
+
+def ep_share_section(steps):
+    """One node's 4-of-16 expert-parallel share (experts 4s..4s+3, s = 0..3)
+    at T = 1, 4, 8: routing from the full 16-way logits, only the local
+    experts computed.  Each share holds 4 independently seeded layers and the
+    timed steps rotate over them, so no weight byte is re-read within 1.5 GB
+    (the 256 MB last-level cache cannot serve repeats)."""
+    import torch
+    import moe_inputs as mi
+    import paper_2506_23635_amd as moe
+    sw = mi.WORKLOADS["ep_share"]
+    n_rot = 4
+    expert_bytes = 3 * sw.d * sw.f * 2
+    staging = torch.empty(3 * sw.d * sw.f, dtype=torch.int16, device="cuda")
+    rows = []
+    for s in range(4):
+        cfg = moe.make_config(sw.d, sw.f, sw.E, sw.k, expert_begin=4 * s, n_local_experts=4,
+                              n_layers=n_rot, max_tokens=8)
+        layer = moe.MoeLayer(cfg)
+        for li in range(n_rot):
+            load_layer_device(layer, sw, li, li, staging)
+        torch.cuda.synchronize()
+        for T in (1, 4, 8):
+            x = torch.empty(T * sw.d, dtype=torch.int16, device="cuda")
+            mi.gen_bf16_device(sw.seed, mi.stream_id(mi.KIND_X), T * sw.d, sw.sigma_x, x.data_ptr(),
+                               layer.stream)
+            x = x.view(T, sw.d)
+            y = torch.empty((T, sw.d), dtype=torch.int16, device="cuda")
+            touched = []
+            for li in range(n_rot):
+                rt = layer.routing_tensors(layer.route(li, x))
+                touched.append(int((rt["counts"][4 * s: 4 * s + 4] > 0).sum()))
+            for i in range(2 * n_rot):
+                layer.forward(i % n_rot, x, y)
+            torch.cuda.synchronize()
+            n = steps - steps % n_rot
+            t0 = time.perf_counter()
+            for i in range(n):
+                layer.forward(i % n_rot, x, y)
+            torch.cuda.synchronize()
+            ms = (time.perf_counter() - t0) * 1e3 / n
+            bytes_step = sum(touched) / n_rot * expert_bytes
+            rows.append({"share": s, "experts": [4 * s, 4 * s + 3], "T": T,
+                         "local_experts_touched": touched, "us_per_step": ms * 1e3,
+                         "hbm_gbs": (bytes_step / (ms * 1e-3) / 1e9) if bytes_step else None})
+            log(f"ep share {s} T={T}: {ms * 1e3:.1f} us, touched {touched}")
+        layer.close()
+        del layer
+    del staging
+    torch.cuda.empty_cache()
+    return rows
+
+
+def stack_section(steps, warmup):
+    """32 chained layers, all 16 experts of every layer resident (203 GB), 4
+    decode tokens: moe_forward_stack timed as HIP graph replays."""
+    import torch
+    import moe_inputs as mi
+    import paper_2506_23635_amd as moe
+    sw = mi.WORKLOADS["stack"]
+    free, _ = torch.cuda.mem_get_info()
+    expert_bytes = 3 * sw.d * sw.f * 2
+    need = sw.n_layers * sw.E * expert_bytes + (8 << 30)
+    if free < need:
+        log(f"stack: skipped ({free / 1e9:.0f} GB free, {need / 1e9:.0f} GB needed)")
+        return None
+    cfg = moe.make_config(sw.d, sw.f, sw.E, sw.k, n_layers=sw.n_layers, max_tokens=sw.T)
+    layer = moe.MoeLayer(cfg)
+    staging = torch.empty(3 * sw.d * sw.f, dtype=torch.int16, device="cuda")
+    t0 = time.perf_counter()
+    for li in range(sw.n_layers):
+        load_layer_device(layer, sw, li, li, staging)
+    torch.cuda.synchronize()
+    log(f"stack: 32 layers generated and prestacked in {time.perf_counter() - t0:.1f} s")
+    del staging
+    x0 = torch.empty(sw.T * sw.d, dtype=torch.int16, device="cuda")
+    mi.gen_bf16_device(sw.seed, mi.stream_id(mi.KIND_X), sw.T * sw.d, sw.sigma_x, x0.data_ptr(),
+                       layer.stream)
+    x0 = x0.view(sw.T, sw.d)
+    # touched experts per layer along the chain (for the traffic figure)
+    touched = []
+    cur = x0.clone()
+    y = torch.empty_like(cur)
+    for li in range(sw.n_layers):
+        rt = layer.routing_tensors(layer.route(li, cur))
+        touched.append(int((rt["counts"] > 0).sum()))
+        layer.forward(li, cur, y)
+        cur = bf16_residual(cur, y)
+    xs = x0.clone()
+
+    def step():
+        xs.copy_(x0)
+        layer.forward_stack(xs)
+
+    for _ in range(warmup):
+        step()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(steps):
+        step()
+    torch.cuda.synchronize()
+    ms_direct = (time.perf_counter() - t0) * 1e3 / steps
+    ms_graph = graph_ms(step, steps, warmup)
+    ms = ms_graph
+    bytes_step = sum(touched) * expert_bytes + sw.n_layers * sw.d * sw.E * 4
+    out = {"workload": "dbrx_moe_stack_32_layers", "T": sw.T, "n_layers": sw.n_layers,
+           "resident_gb": sw.n_layers * sw.E * expert_bytes / 1e9,
+           "ms_per_step": ms, "ms_per_step_direct_launch": ms_direct,
+           "tokens_per_s": sw.T / (ms * 1e-3), "touched_experts_per_layer": touched,
+           "hbm_gb_per_step": bytes_step / 1e9, "hbm_gbs": bytes_step / (ms * 1e-3) / 1e9,
+           "hbm_frac": bytes_step / (ms * 1e-3) / 1e9 / HBM_PEAK_GBS}
+    log(f"stack: {ms:.2f} ms/step graph, {ms_direct:.2f} direct, {out['hbm_gbs']:.0f} GB/s")
+    layer.close()
+    del layer, x0, xs, cur, y
+    torch.cuda.empty_cache()
+    return out
+
+
 def measured_traffic(kernel="decode_gateup", source="moe_decode.hip"):
     """HBM bytes per launch of the dominant kernel from the committed counter
     summary (raw fabric read/write requests), or None when the kernel source
@@ -142,6 +316,9 @@ def main():
     ap.add_argument("--prefill-steps", type=int, default=20)
     ap.add_argument("--no-prefill", action="store_true")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-ep-share", action="store_true")
+    ap.add_argument("--no-stack", action="store_true")
+    ap.add_argument("--stack-steps", type=int, default=20)
     ap.add_argument("--prefill-only", action="store_true",
                     help="time only the prefill layer (for counter collection)")
     ap.add_argument("--calibrate-copy", action="store_true",
@@ -226,6 +403,16 @@ def main():
         del player, px
         torch.cuda.empty_cache()
 
+    ep_share = None
+    if not args.no_ep_share:
+        log("timing the expert-parallel shares ...")
+        ep_share = ep_share_section(args.steps)
+
+    stack = None
+    if not args.no_stack:
+        log("setup and timing of the 32-layer stack ...")
+        stack = stack_section(args.stack_steps, 3)
+
     cpu = None
     if not args.no_cpu_baseline:
         log("timing the CPU oracle ...")
@@ -258,6 +445,8 @@ def main():
         "profile_dropped": dropped,
         "cpu_baseline": cpu,
         "prefill": prefill,
+        "ep_share": ep_share,
+        "stack": stack,
     }
     print(json.dumps(out), flush=True)
 

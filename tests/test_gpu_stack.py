@@ -1,0 +1,80 @@
+"""The 32-layer DBRX stack on 4 decode tokens: all 16 experts of every layer
+resident in one prestacked arena (203 GB; the paper's Sec. "Expert-wise
+Weights Prestacking"), chained by x_{l+1} = bf16(x_l + y_l) through
+moe_forward_stack.
+
+The oracle cannot afford to regenerate the ~350 experts the chain touches, so
+the check is teacher-forced: the chain is replayed layer by layer through
+moe_forward and the oracle's residual add, the replay must equal
+moe_forward_stack bit for bit, and sampled layers are compared with the oracle
+on the GPU's own input to that layer.  Weights come from the device generator
+(bit-equal to the host generator, checked in test_gpu_tiny)."""
+import numpy as np
+import pytest
+
+import moe_inputs as mi
+import oracle
+from harness import check_layer_output, load_workload_device, make_layer, to_np_u16
+
+pytestmark = pytest.mark.gpu
+
+STACK = mi.WORKLOADS["stack"]
+SAMPLED = (0, 13, 31)
+
+
+@pytest.fixture(scope="module")
+def torch_mod():
+    import torch
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    torch.cuda.empty_cache()
+    free, _ = torch.cuda.mem_get_info()
+    if free < 215e9:
+        pytest.skip(f"the 32-layer stack needs ~215 GB of device memory, {free / 1e9:.0f} GB free")
+    return torch
+
+
+@pytest.fixture(scope="module")
+def stack_layer(torch_mod):
+    layer = make_layer(STACK, max_tokens=STACK.T)
+    staging = None
+    for li in range(STACK.n_layers):
+        staging = load_workload_device(layer, STACK, layer_idx=li, staging=staging)
+    del staging
+    yield layer
+    layer.close()
+
+
+def test_stack_matches_layerwise_replay_and_oracle(torch_mod, stack_layer):
+    torch = torch_mod
+    x0 = STACK.x()
+    x_t = torch.from_numpy(x0.view(np.int16)).cuda()
+    stack_layer.forward_stack(x_t)
+    torch.cuda.synchronize()
+    got = to_np_u16(x_t)
+
+    cur = x0
+    inputs, outputs = {}, {}
+    y_t = torch.empty((STACK.T, STACK.d), dtype=torch.int16, device="cuda")
+    for li in range(STACK.n_layers):
+        xin = torch.from_numpy(cur.view(np.int16)).cuda()
+        stack_layer.forward(li, xin, y_t)
+        torch.cuda.synchronize()
+        y = to_np_u16(y_t)
+        if li in SAMPLED:
+            inputs[li], outputs[li] = cur.copy(), y
+        cur = oracle.residual_add(cur, y)
+    # the chained call is the same computation as the per-layer replay
+    assert np.array_equal(got, cur)
+    assert not np.array_equal(got, x0)
+
+    for li in SAMPLED:
+        x = inputs[li]
+        lg = oracle.router_logits(x, STACK.router(li))
+        idx, w = oracle.route_from_logits(lg, STACK.k)
+        touched = sorted(set(idx.reshape(-1).tolist()))
+        G, U, D = [None] * STACK.E, [None] * STACK.E, [None] * STACK.E
+        for e in touched:
+            G[e], U[e], D[e] = STACK.gate(e, li), STACK.up(e, li), STACK.down(e, li)
+        y64, _ = oracle.layer_with_routing(x, idx, w, G, U, D)
+        check_layer_output(outputs[li], y64)
