@@ -37,13 +37,12 @@ constexpr int kRouteWaves = kRouteThreads / kWave;
 constexpr int kMaxK = 8;
 
 template <int kMaxE>
-__device__ inline void select_token(const float* l, int t, int E, int k, const RouteView& rv)
+__device__ inline void select_token(const float* l, int E, int k, int* ids, float* w)
 {
     float lv[kMaxE];
 #pragma unroll
     for (int e = 0; e < kMaxE; ++e) lv[e] = e < E ? l[e] : 0.f;
     uint64_t taken = 0;
-    int ids[kMaxK];
     float ps[kMaxK];
     float lmax = 0.f, z = 0.f;
     for (int j = 0; j < k; ++j) {
@@ -58,27 +57,37 @@ __device__ inline void select_token(const float* l, int t, int E, int k, const R
         if (j == 0) lmax = bv;
         const float p = expf(bv - lmax);
         z += p;
-        rv.topk_idx[(int64_t)t * k + j] = best;
+        ids[j] = best;
 #pragma unroll
         for (int q = 0; q < kMaxK; ++q)
-            if (q == j) { ids[q] = best; ps[q] = p; }
-        if (j >= kMaxK) rv.topk_w[(int64_t)t * k + j] = p;   // normalised below
+            if (q == j) ps[q] = p;
+        if (j >= kMaxK) w[j] = p;   // normalised below
     }
     const float inv = 1.0f / z;
 #pragma unroll
     for (int q = 0; q < kMaxK; ++q)
-        if (q < k) rv.topk_w[(int64_t)t * k + q] = ps[q] * inv;
-    for (int j = kMaxK; j < k; ++j) {
-        float* pw = rv.topk_w + (int64_t)t * k + j;
-        *pw = *pw * inv;
-    }
-    (void)ids;
+        if (q < k) w[q] = ps[q] * inv;
+    for (int j = kMaxK; j < k; ++j) w[j] = w[j] * inv;
 }
 
+// selection of token t into the routing view
 __device__ inline void select_token_any(const float* l, int t, int E, int k, const RouteView& rv)
 {
-    if (E <= 16) select_token<16>(l, t, E, k, rv);
-    else select_token<64>(l, t, E, k, rv);
+    int* ids = rv.topk_idx + (int64_t)t * k;
+    float* w = rv.topk_w + (int64_t)t * k;
+    if (E <= 16) select_token<16>(l, E, k, ids, w);
+    else select_token<64>(l, E, k, ids, w);
+}
+
+// barrier for LDS traffic only: waits for this wave's LDS operations, not for
+// its outstanding global stores (which a __syncthreads() release would)
+__device__ __forceinline__ void lds_barrier()
+{
+    constexpr int kWaitLgkm = 0xC07F;   // lgkmcnt 0; vmcnt and expcnt at their maxima
+    asm volatile("" ::: "memory");
+    __builtin_amdgcn_s_waitcnt(kWaitLgkm);
+    __builtin_amdgcn_s_barrier();
+    asm volatile("" ::: "memory");
 }
 
 __device__ inline void fma8(double& acc, const u32x4_t xv, const float4 w0, const float4 w1)
@@ -96,14 +105,15 @@ __device__ inline void fma8(double& acc, const u32x4_t xv, const float4 w0, cons
 constexpr int kSmallT = 16;
 
 // Decode routing (T <= 16, E <= 16, T*k <= 64): the logits are spread over
-// n_wg workgroups, each owning d/n_wg of the reduction axis (one 8-wide group
-// per thread, thread = (expert tid%16, group tid/16)).  Per workgroup the
+// n_wg workgroups, each owning d/n_wg of the reduction axis (8-wide groups,
+// thread = (expert tid%16, group tid/16)).  Per workgroup the
 // partials are reduced in fixed order (lane butterfly, then over the 16 waves
 // through LDS) and written to the workspace; the workgroup that takes the last
 // ticket of a device-scope counter sums the n_wg partials in workgroup order,
 // selects, weighs and permutes, and rewinds the counter for the next call.
 constexpr int kDecE = 16;
 constexpr int kDecPairs = 64;
+constexpr int kDecMaxWg = 16;   // partial sums read in one batch (d <= 8192)
 
 struct DecodeRouteArgs {
     const uint16_t* x;
@@ -120,6 +130,8 @@ __global__ __launch_bounds__(kRouteThreads) void route_decode_kernel(DecodeRoute
     __shared__ double wsum[kRouteWaves][kSmallT][kDecE];
     __shared__ float lg[kSmallT][kDecE];
     __shared__ int s_ids[kDecPairs];
+    __shared__ float s_w[kDecPairs];
+    __shared__ int s_rank[kSmallT][kDecE];
     __shared__ int s_cnt[kDecE];
     __shared__ int s_off[kDecE + 1];
     __shared__ int s_last;
@@ -127,11 +139,13 @@ __global__ __launch_bounds__(kRouteThreads) void route_decode_kernel(DecodeRoute
     const int tid = threadIdx.x;
     const int lane = tid & 63, wid = tid >> 6;
     const int e = tid & 15;
-    const int g = blockIdx.x * (kRouteThreads / kDecE) + (tid >> 4);
     double acc[kSmallT];
 #pragma unroll
     for (int t = 0; t < kSmallT; ++t) acc[t] = 0.0;
-    if (e < E && g < d / 8) {
+    // 8-element groups blockIdx*64 + tid/16, then + n_wg*64, ... (one pass
+    // when the grid covers d, several for a single workgroup)
+    for (int g = blockIdx.x * (kRouteThreads / kDecE) + (tid >> 4); e < E && g < d / 8;
+         g += a.n_wg * (kRouteThreads / kDecE)) {
         const float4 w0 = *reinterpret_cast<const float4*>(a.wrT + (int64_t)e * d + g * 8);
         const float4 w1 = *reinterpret_cast<const float4*>(a.wrT + (int64_t)e * d + g * 8 + 4);
 #pragma unroll
@@ -162,26 +176,72 @@ __global__ __launch_bounds__(kRouteThreads) void route_decode_kernel(DecodeRoute
     __syncthreads();
     if (!s_last) return;
     __threadfence();
+    // the last workgroup: logits, selection and permutation in LDS, then
+    // every routing output written at the end (global stores are not waited
+    // for inside the workgroup).  Every step is spread over threads: one
+    // (token, expert) pair per thread.
     if (tid < T * kDecE) {
         const int t = tid / kDecE, ee = tid % kDecE;
         if (ee < E) {
+            // the partials of all workgroups loaded at once, summed in
+            // workgroup order
+            double pv[kDecMaxWg];
+#pragma unroll
+            for (int w = 0; w < kDecMaxWg; ++w)
+                pv[w] = w < a.n_wg ? __builtin_nontemporal_load(
+                                         &a.partial[((int64_t)w * kSmallT + t) * kDecE + ee])
+                                   : 0.0;
             double v = 0.0;
-            for (int w = 0; w < a.n_wg; ++w)
+#pragma unroll
+            for (int w = 0; w < kDecMaxWg; ++w)
+                if (w < a.n_wg) v += pv[w];
+            for (int w = kDecMaxWg; w < a.n_wg; ++w)
                 v += __builtin_nontemporal_load(&a.partial[((int64_t)w * kSmallT + t) * kDecE + ee]);
             float l = (float)v;
             if (a.bias) l = __fadd_rn(l, a.bias[ee]);
             lg[t][ee] = l;
-            a.rv.logits[(int64_t)t * E + ee] = l;
         }
     }
     if (tid == 0) *a.counter = 0u;
-    __syncthreads();
-    // selection (one thread per token); ids also kept in LDS
-    if (tid < T) {
-        select_token<kDecE>(&lg[tid][0], tid, E, k, a.rv);
-        for (int j = 0; j < k; ++j) s_ids[tid * k + j] = a.rv.topk_idx[(int64_t)tid * k + j];
+    lds_barrier();
+    // rank of expert e in its token's order (logit descending, id ascending):
+    // the experts before e with a logit >= its own and those after it with a
+    // larger one; rank < k selects it at slot rank.  A row holding a NaN
+    // takes the sequential scan instead (its order is scan-dependent).
+    if (tid < T * kDecE) {
+        const int t = tid / kDecE, e = tid % kDecE;
+        if (e < E) {
+            const float le = lg[t][e];
+            int r = 0;
+            bool ordered = true;
+            for (int q = 0; q < E; ++q) {
+                const float lq = lg[t][q];
+                ordered = ordered && lq == lq;
+                r += q < e ? (lq >= le ? 1 : 0) : (lq > le ? 1 : 0);
+            }
+            s_rank[t][e] = ordered ? r : -1;
+            if (ordered && r < k) s_ids[t * k + r] = e;
+        }
     }
-    __syncthreads();
+    lds_barrier();
+    if (tid < T) {
+        const int t = tid;
+        if (s_rank[t][0] < 0) {
+            select_token<kDecE>(&lg[t][0], E, k, &s_ids[t * k], &s_w[t * k]);
+        } else {
+            // weights in slot order, as the sequential selection forms them
+            const float lmax = lg[t][s_ids[t * k]];
+            float z = 0.f;
+            for (int j2 = 0; j2 < k; ++j2) {
+                const float p = expf(lg[t][s_ids[t * k + j2]] - lmax);
+                s_w[t * k + j2] = p;
+                z += p;
+            }
+            const float inv = 1.0f / z;
+            for (int j2 = 0; j2 < k; ++j2) s_w[t * k + j2] = s_w[t * k + j2] * inv;
+        }
+    }
+    lds_barrier();
     const int P = T * k;
     const int lo = a.e_begin, hi = a.e_begin + a.n_local;
     if (tid < E) {
@@ -190,32 +250,45 @@ __global__ __launch_bounds__(kRouteThreads) void route_decode_kernel(DecodeRoute
             for (int p = 0; p < P; ++p) c += (s_ids[p] == tid);
         s_cnt[tid] = c;
     }
-    __syncthreads();
-    if (tid == 0) {
-        int run = 0, na = 0, nt = 0;
-        for (int ee = 0; ee < E; ++ee) {
-            const int c = s_cnt[ee];
-            s_off[ee] = run;
-            a.rv.counts[ee] = c;
-            a.rv.offsets[ee] = run;
+    lds_barrier();
+    // per expert: its first row, active-list slot and first tile, from
+    // prefix sums over the experts before it (lanes 0..15 of wave 0)
+    if (wid == 0) {
+        const int c = tid < E ? s_cnt[tid] : 0;
+        const int nz = c > 0 ? 1 : 0;
+        const int tl = (c + a.tile_rows - 1) / a.tile_rows;
+        int run = c, na = nz, nt = tl;
+#pragma unroll
+        for (int off = 1; off < kDecE; off <<= 1) {
+            const int r1 = __shfl_up(run, off, 64), n1 = __shfl_up(na, off, 64),
+                      t1 = __shfl_up(nt, off, 64);
+            if (lane >= off) { run += r1; na += n1; nt += t1; }
+        }
+        run -= c; na -= nz; nt -= tl;   // exclusive
+        if (tid < E) {
+            s_off[tid] = run;
+            a.rv.counts[tid] = c;
+            a.rv.offsets[tid] = run;
             if (c > 0) {
-                a.rv.active[1 + na++] = ee;
+                a.rv.active[1 + na] = tid;
                 for (int r = 0; r < c; r += a.tile_rows) {
-                    a.rv.tiles[2 * nt] = ee;
+                    a.rv.tiles[2 * nt] = tid;
                     a.rv.tiles[2 * nt + 1] = run + r;
                     ++nt;
                 }
             }
-            run += c;
+            if (tid == E - 1) {
+                a.rv.offsets[E] = run + c;
+                a.rv.active[0] = na + nz;
+                *a.rv.n_tiles = nt;
+            }
         }
-        s_off[E] = run;
-        a.rv.offsets[E] = run;
-        a.rv.active[0] = na;
-        *a.rv.n_tiles = nt;
     }
-    __syncthreads();
+    lds_barrier();
     if (tid < P) {
         const int ee = s_ids[tid];
+        a.rv.topk_idx[tid] = ee;
+        a.rv.topk_w[tid] = s_w[tid];
         if (ee >= lo && ee < hi) {
             int rank = 0;
             for (int p = 0; p < tid; ++p) rank += (s_ids[p] == ee);
@@ -225,6 +298,10 @@ __global__ __launch_bounds__(kRouteThreads) void route_decode_kernel(DecodeRoute
         } else {
             a.rv.pair_row[tid] = -1;
         }
+    }
+    if (tid < T * kDecE) {
+        const int t = tid / kDecE, ee = tid % kDecE;
+        if (ee < E) a.rv.logits[(int64_t)t * E + ee] = lg[t][ee];
     }
 }
 
@@ -303,7 +380,7 @@ __global__ __launch_bounds__(kRsThreads) void router_select_kernel(const uint16_
                 }
         }
     }
-    __syncthreads();
+    lds_barrier();
     if (threadIdx.x < kRsTok) {
         const int t = blockIdx.x * kRsTok + threadIdx.x;
         if (t < T) select_token_any(&lg[threadIdx.x][0], t, E, k, rv);
@@ -347,12 +424,12 @@ __global__ __launch_bounds__(kRouteThreads) void permute_kernel(PermArgs a)
     const int lo = a.e_begin, hi = a.e_begin + a.n_local;
     const RouteView& rv = a.rv;
     if (tid < 64) hist[tid] = 0;
-    __syncthreads();
+    lds_barrier();
     for (int p = tid; p < P; p += kRouteThreads) {
         const int e = rv.topk_idx[p];
         if (e >= lo && e < hi) atomicAdd(&hist[e], 1);
     }
-    __syncthreads();
+    lds_barrier();
     if (tid == 0) {
         int run = 0, na = 0, nt = 0;
         for (int e = 0; e < E; ++e) {
@@ -374,7 +451,7 @@ __global__ __launch_bounds__(kRouteThreads) void permute_kernel(PermArgs a)
         rv.active[0] = na;
         *rv.n_tiles = nt;
     }
-    __syncthreads();
+    lds_barrier();
     for (int r0 = 0; r0 < P; r0 += kRouteThreads * kPermChunk) {
         const int p0 = r0 + tid * kPermChunk;
         int ids[kPermChunk];
@@ -394,7 +471,7 @@ __global__ __launch_bounds__(kRouteThreads) void permute_kernel(PermArgs a)
                 if (lane >= off) inc += o;
             }
             if (lane == 63) wtot[wid] = inc;
-            __syncthreads();
+            lds_barrier();
             int before = 0, tot = 0;
             for (int w = 0; w < kRouteWaves; ++w) {
                 const int c = wtot[w];
@@ -410,7 +487,7 @@ __global__ __launch_bounds__(kRouteThreads) void permute_kernel(PermArgs a)
                     ++row;
                 }
             }
-            __syncthreads();   // every thread has read wtot and cursor[e]
+            lds_barrier();   // every thread has read wtot and cursor[e]
             if (tid == 0) cursor[e] += tot;
         }
     }
@@ -437,6 +514,7 @@ extern "C" int moe_route_decode_ok(int T, int E, int k)
 
 extern "C" int moe_route_decode_wgs(int d) { return (d / 8 + 63) / 64; }
 
+
 extern "C" hipError_t moe_launch_zero_counter(unsigned int* counter, hipStream_t s)
 {
     hipLaunchKernelGGL(moe::zero_u32_kernel, dim3(1), dim3(1), 0, s, counter);
@@ -453,8 +531,8 @@ extern "C" hipError_t moe_launch_route_decode(const uint16_t* x, const float* wr
     a.x = x; a.wrT = wrT; a.bias = bias; a.partial = partial; a.counter = counter;
     a.T = T; a.d = d; a.E = E; a.k = k;
     a.e_begin = e_begin; a.n_local = n_local; a.tile_rows = tile_rows;
-    a.n_wg = moe_route_decode_wgs(d);
     a.rv = *rv;
+    a.n_wg = moe_route_decode_wgs(d);
     hipLaunchKernelGGL(moe::route_decode_kernel, dim3(a.n_wg), dim3(moe::kRouteThreads), 0, s, a);
     return hipGetLastError();
 }

@@ -120,6 +120,47 @@ def test_route_from_x_many_tokens(torch_mod, tiny_layer, T):
     _check_routing(got, idx, w, wl.E)
 
 
+@pytest.mark.parametrize("T", [1, 7, 16])
+def test_decode_routing_ties(torch_mod, tiny_layer, T):
+    """A zero router weight makes every logit equal to its expert's bias, so
+    the decode routing must break ties by the lower expert id (and order the
+    slots by logit, then id) exactly like the oracle's scan."""
+    torch = torch_mod
+    layer = make_layer(TINY, max_tokens=16)
+    bias = np.array([0.5, 1.0, 1.0, -0.0, 0.0, 1.0, 0.5, -2.0], dtype=np.float32)
+    layer.load_router(0, torch.zeros(TINY.d * TINY.E, dtype=torch.float32, device="cuda"),
+                      torch.from_numpy(bias).cuda())
+    x_t, x = x_device(TINY.with_(T=T))
+    got = layer.routing_tensors(layer.route(0, x_t))
+    lg = oracle.router_logits(x, np.zeros((TINY.d, TINY.E), np.float32), bias)
+    assert np.array_equal(lg, np.tile(bias, (T, 1)))      # values (0 + -0 is +0)
+    assert np.array_equal(got["logits"].view(np.uint32), lg.view(np.uint32))
+    idx, w = oracle.route_from_logits(lg, TINY.k)
+    _check_routing(got, idx, w, TINY.E)
+    assert idx[0].tolist() == [1, 2]
+    layer.close()
+
+
+def test_decode_routing_nan_token(torch_mod, tiny_layer):
+    """A token whose activations hold a NaN has NaN logits (the oracle rejects
+    such rows, so no reference exists for them): it still gets k distinct
+    valid experts, and the other tokens route exactly as the oracle says."""
+    torch = torch_mod
+    wl = TINY.with_(T=4)
+    x = wl.x().copy()
+    x[2, 5] = 0x7FC0                       # bf16 quiet NaN
+    x_t = torch.from_numpy(x.view(np.int16)).cuda()
+    got = tiny_layer.routing_tensors(tiny_layer.route(0, x_t))
+    assert np.isnan(got["logits"][2]).all()
+    ids = got["idx"][2]
+    assert len(set(ids.tolist())) == wl.k and ids.min() >= 0 and ids.max() < wl.E
+    ok = np.array([0, 1, 3])
+    lg = oracle.router_logits(x[ok], wl.router())
+    idx, w = oracle.route_from_logits(lg, wl.k)
+    assert np.array_equal(got["idx"][ok], idx)
+    assert np.abs(got["w"][ok] - w).max() <= 2e-6
+
+
 # 24 experts, top-6: above the decode routing's limits (16 experts, 64 pairs),
 # so even one token goes through the general router and permutation
 WIDE = TINY.with_(E=24, k=6, T=40)
