@@ -12,7 +12,7 @@
 // Kernels
 //   router_select_kernel: 8 tokens per workgroup, a wave takes 4 tokens x 8
 //       experts, each dot product split over the 64 lanes and summed by a
-//       fixed butterfly; then each token's selection.
+//       fixed transpose-reduce; then each token's selection.
 //   route_decode_kernel (T <= 16, E <= 16, T*k <= 64): the logits spread over
 //       d/512 workgroups, the last one to finish selects and permutes.
 //   select_kernel: selection and weights from caller-supplied fp32 logits.
@@ -312,10 +312,11 @@ __global__ void zero_u32_kernel(unsigned int* p) { *p = 0u; }
 // Lane l accumulates, in fp64, the 8-element groups l, l + 64, ... of the
 // reduction axis for its 4 tokens x 8 experts, so each router value it
 // loads serves 4 tokens and each x value 8 experts, and a wave reads 512
-// consecutive elements of every row per step.  A fixed xor butterfly over
-// the 64 lanes sums the lane partials; lane 0's sums are rounded once to
-// fp32 and the bias added in fp32; then one thread per token selects its
-// experts from the logits in LDS.
+// consecutive elements of every row per step (two steps in flight).  A
+// fixed transpose-reduce over the 64 lanes sums the lane partials (32
+// shuffles for the 32 sums); each sum is rounded once to fp32 and the bias
+// added in fp32; then one thread per token selects its experts from the
+// logits in LDS.
 constexpr int kRsTokWave = 4;
 constexpr int kRsExp = 8;
 constexpr int kRsTok = 2 * kRsTokWave;
@@ -346,38 +347,76 @@ __global__ __launch_bounds__(kRsThreads) void router_select_kernel(const uint16_
         for (int i = 0; i < kRsTokWave; ++i) xr[i] = x + (int64_t)min(t0 + i, T - 1) * d;
 #pragma unroll
         for (int j = 0; j < kRsExp; ++j) wr[j] = wrT + (int64_t)min(e0 + j, E - 1) * d;
-        for (int g = lane * 8; g < d; g += kWave * 8) {
+        // two steps of loads in flight: step g + 512 is fetched while step g
+        // computes (a prefetch past d re-reads the lane's current step)
+        struct Step {
             u32x4_t xv[kRsTokWave];
+            float4 w0[kRsExp], w1[kRsExp];
+        };
+        auto fetch = [&](Step& st, int g) {
 #pragma unroll
-            for (int i = 0; i < kRsTokWave; ++i) xv[i] = *reinterpret_cast<const u32x4_t*>(xr[i] + g);
+            for (int i = 0; i < kRsTokWave; ++i) st.xv[i] = *reinterpret_cast<const u32x4_t*>(xr[i] + g);
 #pragma unroll
             for (int j = 0; j < kRsExp; ++j) {
-                const float4 w0 = *reinterpret_cast<const float4*>(wr[j] + g);
-                const float4 w1 = *reinterpret_cast<const float4*>(wr[j] + g + 4);
-#pragma unroll
-                for (int i = 0; i < kRsTokWave; ++i) fma8(acc[i][j], xv[i], w0, w1);
+                st.w0[j] = *reinterpret_cast<const float4*>(wr[j] + g);
+                st.w1[j] = *reinterpret_cast<const float4*>(wr[j] + g + 4);
             }
-        }
-#pragma unroll
-        for (int i = 0; i < kRsTokWave; ++i)
+        };
+        auto fma_step = [&](const Step& st) {
 #pragma unroll
             for (int j = 0; j < kRsExp; ++j)
 #pragma unroll
-                for (int off = kWave / 2; off >= 1; off >>= 1)
-                    acc[i][j] += __shfl_xor(acc[i][j], off, kWave);
-        if (lane == 0) {
+                for (int i = 0; i < kRsTokWave; ++i) fma8(acc[i][j], st.xv[i], st.w0[j], st.w1[j]);
+        };
+        constexpr int kStep = kWave * 8;
+        Step s0, s1;
+        int g = lane * 8;
+        if (g < d) fetch(s0, g);
+        for (; g < d; g += 2 * kStep) {
+            const bool more = g + kStep < d;
+            fetch(s1, more ? g + kStep : g);
+            fma_step(s0);
+            if (!more) break;
+            const bool more2 = g + 2 * kStep < d;
+            fetch(s0, more2 ? g + 2 * kStep : g);
+            fma_step(s1);
+        }
+        // transpose-reduce over the 64 lanes: at the step with lane offset o
+        // a lane keeps half of its n values (the upper half if its o bit is
+        // set), sends the other half to lane ^ o and adds what it receives;
+        // after offsets 32..2 each lane holds one value summed over 32 lanes,
+        // and offset 1 completes it.  Value q = 8 i + j ends on the lanes whose
+        // bits 5..1 spell q (bit 5 most significant).  Fixed order.
+        constexpr int kVals = kRsTokWave * kRsExp;   // 32
+        double v[kVals];
 #pragma unroll
-            for (int i = 0; i < kRsTokWave; ++i)
+        for (int i = 0; i < kRsTokWave; ++i)
 #pragma unroll
-                for (int j = 0; j < kRsExp; ++j) {
-                    const int t = t0 + i, e = e0 + j;
-                    if (t < T && e < E) {
-                        float v = (float)acc[i][j];
-                        if (bias) v = __fadd_rn(v, bias[e]);
-                        lg[tg * kRsTokWave + i][e] = v;
-                        rv.logits[(int64_t)t * E + e] = v;
-                    }
+            for (int j = 0; j < kRsExp; ++j) v[i * kRsExp + j] = acc[i][j];
+#pragma unroll
+        for (int o = kWave / 2, n = kVals; o >= 2; o >>= 1, n >>= 1) {
+            const bool up = (lane & o) != 0;
+#pragma unroll
+            for (int m = 0; m < kVals / 2; ++m) {
+                if (m < n / 2) {
+                    const double send = up ? v[m] : v[m + n / 2];
+                    const double keep = up ? v[m + n / 2] : v[m];
+                    v[m] = keep + __shfl_xor(send, o, kWave);
                 }
+            }
+        }
+        const double total = v[0] + __shfl_xor(v[0], 1, kWave);
+        const int q = ((lane >> 5) & 1) * 16 + ((lane >> 4) & 1) * 8 + ((lane >> 3) & 1) * 4 +
+                      ((lane >> 2) & 1) * 2 + ((lane >> 1) & 1);
+        if ((lane & 1) == 0) {
+            const int i = q / kRsExp, j = q % kRsExp;
+            const int t = t0 + i, e = e0 + j;
+            if (t < T && e < E) {
+                float lv = (float)total;
+                if (bias) lv = __fadd_rn(lv, bias[e]);
+                lg[tg * kRsTokWave + i][e] = lv;
+                rv.logits[(int64_t)t * E + e] = lv;
+            }
         }
     }
     lds_barrier();
@@ -404,10 +443,12 @@ __global__ __launch_bounds__(256) void select_kernel(const float* __restrict__ l
 //  1. counts: LDS histogram of the local pairs (order-free); thread 0 then
 //     writes counts, offsets, the active-expert list and the GEMM tile list.
 //  2. rows: pairs in rounds of 1024 x 8; each thread holds 8 consecutive
-//     pairs; per local expert, a wave scan of the per-thread counts plus the
-//     wave totals (LDS) give each pair its row after the expert's cursor.
+//     pairs; per group of 16 experts, one wave scan of packed per-thread
+//     counts plus a scan of the wave totals give each pair its row after the
+//     expert's cursor.
 // Deterministic: no atomic decides a row.
 constexpr int kPermChunk = 8;
+constexpr int kPermGroup = 16;   // experts counted together (packed counters)
 
 struct PermArgs {
     int T, E, k, e_begin, n_local, tile_rows;
@@ -416,9 +457,12 @@ struct PermArgs {
 
 __global__ __launch_bounds__(kRouteThreads) void permute_kernel(PermArgs a)
 {
+    constexpr int kWords = kPermGroup / 2;   // two 16-bit counters per word
     __shared__ int hist[64];
     __shared__ int cursor[64];
-    __shared__ int wtot[kRouteWaves];
+    __shared__ uint32_t wtot[kRouteWaves][kWords];
+    __shared__ uint32_t wpre[kRouteWaves][kWords];
+    __shared__ uint32_t rtot[kWords];
     const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
     const int E = a.E, k = a.k, P = a.T * a.k;
     const int lo = a.e_begin, hi = a.e_begin + a.n_local;
@@ -430,28 +474,45 @@ __global__ __launch_bounds__(kRouteThreads) void permute_kernel(PermArgs a)
         if (e >= lo && e < hi) atomicAdd(&hist[e], 1);
     }
     lds_barrier();
-    if (tid == 0) {
-        int run = 0, na = 0, nt = 0;
-        for (int e = 0; e < E; ++e) {
-            const int c = hist[e];
-            rv.counts[e] = c;
-            rv.offsets[e] = run;
-            cursor[e] = run;
+    // offsets, active list and tiles: prefix sums over the experts (wave 0)
+    if (wid == 0) {
+        int c = lane < E ? hist[lane] : 0;
+        const int nz = c > 0 ? 1 : 0;
+        const int tl = (c + a.tile_rows - 1) / a.tile_rows;
+        int run = c, na = nz, nt = tl;
+#pragma unroll
+        for (int off = 1; off < 64; off <<= 1) {
+            const int r1 = __shfl_up(run, off, 64), n1 = __shfl_up(na, off, 64),
+                      t1 = __shfl_up(nt, off, 64);
+            if (lane >= off) { run += r1; na += n1; nt += t1; }
+        }
+        run -= c; na -= nz; nt -= tl;   // exclusive
+        if (lane < E) {
+            rv.counts[lane] = c;
+            rv.offsets[lane] = run;
+            cursor[lane] = run;
             if (c > 0) {
-                rv.active[1 + na++] = e;
+                rv.active[1 + na] = lane;
                 for (int r = 0; r < c; r += a.tile_rows) {
-                    rv.tiles[2 * nt] = e;
+                    rv.tiles[2 * nt] = lane;
                     rv.tiles[2 * nt + 1] = run + r;
                     ++nt;
                 }
             }
-            run += c;
+            if (lane == E - 1) {
+                rv.offsets[E] = run + c;
+                rv.active[0] = na + nz;
+                *rv.n_tiles = nt;
+            }
         }
-        rv.offsets[E] = run;
-        rv.active[0] = na;
-        *rv.n_tiles = nt;
     }
     lds_barrier();
+    // rows: rounds of 1024 x 8 pairs; thread t holds pairs 8t .. 8t+7 of the
+    // round.  Per group of 16 experts, each thread packs its per-expert counts
+    // two to a word (a round has at most 8192 pairs, below 2^16), one
+    // wave-level scan and one scan over the wave totals give every thread the
+    // rows of its pairs: cursor[e] + pairs of expert e in earlier threads +
+    // earlier pairs of its own.
     for (int r0 = 0; r0 < P; r0 += kRouteThreads * kPermChunk) {
         const int p0 = r0 + tid * kPermChunk;
         int ids[kPermChunk];
@@ -460,35 +521,71 @@ __global__ __launch_bounds__(kRouteThreads) void permute_kernel(PermArgs a)
             ids[q] = p0 + q < P ? rv.topk_idx[p0 + q] : -1;
             if (p0 + q < P && (ids[q] < lo || ids[q] >= hi)) rv.pair_row[p0 + q] = -1;
         }
-        for (int e = lo; e < hi; ++e) {
-            int cnt = 0;
+        for (int g0 = lo - lo % kPermGroup; g0 < hi; g0 += kPermGroup) {
+            uint32_t c[kWords];
 #pragma unroll
-            for (int q = 0; q < kPermChunk; ++q) cnt += ids[q] == e ? 1 : 0;
-            int inc = cnt;
-#pragma unroll
-            for (int off = 1; off < 64; off <<= 1) {
-                const int o = __shfl_up(inc, off, 64);
-                if (lane >= off) inc += o;
-            }
-            if (lane == 63) wtot[wid] = inc;
-            lds_barrier();
-            int before = 0, tot = 0;
-            for (int w = 0; w < kRouteWaves; ++w) {
-                const int c = wtot[w];
-                before += w < wid ? c : 0;
-                tot += c;
-            }
-            int row = cursor[e] + before + inc - cnt;
+            for (int m = 0; m < kWords; ++m) c[m] = 0u;
 #pragma unroll
             for (int q = 0; q < kPermChunk; ++q) {
-                if (ids[q] == e) {
+                const int rel = ids[q] - g0;
+                const bool mine = ids[q] >= lo && ids[q] < hi && rel >= 0 && rel < kPermGroup;
+#pragma unroll
+                for (int m = 0; m < kWords; ++m)
+                    if (mine && (rel >> 1) == m) c[m] += 1u << (16 * (rel & 1));
+            }
+            uint32_t inc[kWords];
+#pragma unroll
+            for (int m = 0; m < kWords; ++m) {
+                uint32_t v = c[m];
+#pragma unroll
+                for (int off = 1; off < 64; off <<= 1) {
+                    const uint32_t o = __shfl_up(v, off, 64);
+                    if (lane >= off) v += o;
+                }
+                inc[m] = v;
+            }
+            if (lane == 63) {
+#pragma unroll
+                for (int m = 0; m < kWords; ++m) wtot[wid][m] = inc[m];
+            }
+            lds_barrier();
+            if (tid < kRouteWaves * kWords) {
+                const int w = tid / kWords, m = tid % kWords;
+                uint32_t pre = 0u;
+                for (int w2 = 0; w2 < w; ++w2) pre += wtot[w2][m];
+                wpre[w][m] = pre;
+                if (w == kRouteWaves - 1) rtot[m] = pre + wtot[w][m];
+            }
+            lds_barrier();
+            // exclusive count of each expert's pairs before this thread's
+            uint32_t ex[kWords];
+#pragma unroll
+            for (int m = 0; m < kWords; ++m) ex[m] = wpre[wid][m] + inc[m] - c[m];
+            uint32_t own[kWords];
+#pragma unroll
+            for (int m = 0; m < kWords; ++m) own[m] = 0u;
+#pragma unroll
+            for (int q = 0; q < kPermChunk; ++q) {
+                const int rel = ids[q] - g0;
+                const bool mine = ids[q] >= lo && ids[q] < hi && rel >= 0 && rel < kPermGroup;
+                if (mine) {
+                    uint32_t before = 0u;
+#pragma unroll
+                    for (int m = 0; m < kWords; ++m)
+                        if ((rel >> 1) == m) {
+                            const int sh = 16 * (rel & 1);
+                            before = ((ex[m] >> sh) & 0xFFFFu) + ((own[m] >> sh) & 0xFFFFu);
+                            own[m] += 1u << sh;
+                        }
+                    const int row = cursor[ids[q]] + (int)before;
                     rv.pair_row[p0 + q] = row;
                     rv.row_token[row] = (p0 + q) / k;
-                    ++row;
                 }
             }
-            lds_barrier();   // every thread has read wtot and cursor[e]
-            if (tid == 0) cursor[e] += tot;
+            lds_barrier();   // every thread has read cursor and wpre
+            if (tid < kPermGroup && g0 + tid >= lo && g0 + tid < hi)
+                cursor[g0 + tid] += (int)((rtot[tid >> 1] >> (16 * (tid & 1))) & 0xFFFFu);
+            lds_barrier();
         }
     }
 }

@@ -285,6 +285,31 @@ def test_expert_parallel_shares(torch_mod):
     assert rel_l2(total, full["y64"]) <= 2e-3
 
 
+@pytest.mark.parametrize("T", [40, 300])
+def test_expert_parallel_shares_many_tokens(torch_mod, T):
+    """Shares through the many-token routing (router + permutation kernels)
+    and the grouped GEMM: local counts and rows, partial outputs, and the
+    four partials summing to the layer."""
+    torch = torch_mod
+    wl = TINY.with_(T=T)
+    x_t, x = x_device(wl)
+    full = _oracle_full(wl, x)
+    total = np.zeros_like(full["y64"])
+    for s in range(4):
+        layer = make_layer(wl, max_tokens=T, e_begin=2 * s, n_local=2)
+        load_workload_host(layer, wl)
+        got = layer.routing_tensors(layer.route(0, x_t))
+        _check_routing(got, full["idx"], full["w"], wl.E, e_begin=2 * s, n_local=2)
+        y = _forward(torch, layer, x_t)
+        ref = _oracle_full(wl, x, e_begin=2 * s, n_local=2)
+        has = np.any((full["idx"] >= 2 * s) & (full["idx"] < 2 * s + 2), axis=1)
+        assert np.all(y[~has] & 0x7FFF == 0)
+        check_layer_output(y[has], ref["y64"][has])
+        total += bf16_f64(y)
+        layer.close()
+    assert rel_l2(total, full["y64"]) <= 2e-3
+
+
 def test_deterministic_bitwise(torch_mod, tiny_layer):
     torch = torch_mod
     for T in (16, 300):
