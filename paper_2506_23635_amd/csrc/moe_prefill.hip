@@ -32,6 +32,8 @@
 //
 // Token tiles (expert, first grouped row) come from the routing kernel; the
 // grid is sized for the worst case and surplus workgroups exit at once.
+#include <type_traits>
+
 #include "moe_common.h"
 
 namespace moe {
@@ -126,26 +128,32 @@ constexpr int a_load_unit(int fb, int j) { return j + 1 < KS ? 8 * (j + 1) + 2 *
 // vector-memory ops issued after the last load of B(s+1) (stage s-1, unit
 // b_load_unit(B_LOADS-1)) up to stage s's barrier; vector-memory ops
 // complete in order, so waiting until at most this many are outstanding
-// means this wave's part of B(s+1) is in LDS
-constexpr int vm_after_last_b()
+// means this wave's part of B(s+1) is in LDS.  The stages after the main
+// loop (kTail) issue no A refills: their registers are never read again, and
+// the compiler would drop them as dead loads anyway.  The stage before a tail
+// stage may be one too, so there only the stage's own B loads before the
+// barrier are certain to follow B(s+1).
+constexpr int vm_after_last_b(bool kTail)
 {
     int n = 0;
+    for (int q = 0; q < B_LOADS; ++q)
+        if (b_load_unit(q) < kBarrierUnit) ++n;
+    if (kTail) return n;
     for (int fb = 0; fb < FB; ++fb)
         for (int j = 0; j < KS; ++j) {
             const int u = a_load_unit(fb, j);
             if (u > b_load_unit(B_LOADS - 1)) ++n;   // rest of stage s-1
             if (u < kBarrierUnit) ++n;               // stage s before the barrier
         }
-    for (int q = 0; q < B_LOADS; ++q)
-        if (b_load_unit(q) < kBarrierUnit) ++n;
     return n;
 }
-constexpr int kAfterB = vm_after_last_b();
 static_assert(b_load_unit(B_LOADS - 1) >= kBarrierUnit, "every B(s+1) load precedes the count");
-static_assert(kAfterB < 64, "vmcnt holds 6 bits");
+static_assert(vm_after_last_b(false) < 64, "vmcnt holds 6 bits");
 // s_waitcnt immediate (gfx9 layout: vmcnt[3:0] | expcnt[6:4] | lgkmcnt[11:8] |
 // vmcnt[15:14])
-constexpr int kWaitBStage = (kAfterB & 0xF) | ((kAfterB >> 4) << 14) | (0x7 << 4) | (0xF << 8);
+constexpr int wait_vm(int n) { return (n & 0xF) | ((n >> 4) << 14) | (0x7 << 4) | (0xF << 8); }
+constexpr int kWaitBStage = wait_vm(vm_after_last_b(false));
+constexpr int kWaitBTail = wait_vm(vm_after_last_b(true));
 
 template <bool kFull>
 __device__ __forceinline__ void tile_loop(const TileCtx& c, int n_pairs, uint8_t* lds,
@@ -183,28 +191,30 @@ __device__ __forceinline__ void tile_loop(const TileCtx& c, int n_pairs, uint8_t
     // explicit partial wait + bare barrier: a __syncthreads() release fence
     // would wait for every outstanding LDS DMA (vmcnt 0); the empty asm
     // statements keep the compiler from moving memory operations across it
-    auto wait_and_barrier = [&]() {
-        __builtin_amdgcn_s_waitcnt(kWaitBStage);
+    auto wait_and_barrier = [&](auto tail) {
+        __builtin_amdgcn_s_waitcnt(decltype(tail)::value ? kWaitBTail : kWaitBStage);
         asm volatile("" ::: "memory");
         __builtin_amdgcn_s_barrier();
         asm volatile("" ::: "memory");
     };
-    // stage s (A in A, B in LDS buffer s % 4).  Loads past the last stage
-    // re-read the last stage into buffers and registers no stage reads.
-    auto stage = [&](int s, u32x4_t (&A)[A_FRAGS]) {
+    // stage s (A in A, B in LDS buffer s % 4).  B loads past the last stage
+    // re-read the last stage into buffers no stage reads; A refills are
+    // issued in the main loop only (tail is std::true_type after it).
+    auto stage = [&](int s, u32x4_t (&A)[A_FRAGS], auto tail) {
+        constexpr bool kTail = decltype(tail)::value;
         const uint8_t* bcur = lds + (s % kRingB) * B_STAGE_BYTES;
         const uint8_t* bnext = lds + ((s + 1) % kRingB) * B_STAGE_BYTES;
         const int sb = min(s + 2, n_stages - 1), bbuf = (s + 2) % kRingB;
         const int sa = min(s + kRingA, n_stages - 1);
 #pragma unroll
         for (int u = 0; u < kUnits; ++u) {
-            if (u == kBarrierUnit) wait_and_barrier();
+            if (u == kBarrierUnit) wait_and_barrier(tail);
             if (u % 4 == 1) load_b1(sb, bbuf, u / 4);
 #pragma unroll
             for (int fb = 0; fb < FB; ++fb)
 #pragma unroll
                 for (int j = 0; j < KS; ++j)
-                    if (a_load_unit(fb, j) == u) load_a1(sa, fb, j, A[fb * KS + j]);
+                    if (!kTail && a_load_unit(fb, j) == u) load_a1(sa, fb, j, A[fb * KS + j]);
             if (u + kLook < kUnits)
                 read_unit(bcur, u + kLook);
             else
@@ -222,7 +232,7 @@ __device__ __forceinline__ void tile_loop(const TileCtx& c, int n_pairs, uint8_t
         for (int fb = 0; fb < FB; ++fb)
 #pragma unroll
             for (int j = 0; j < KS; ++j)
-                if (a_load_unit(fb, j) == kUnits) load_a1(sa, fb, j, A[fb * KS + j]);
+                if (!kTail && a_load_unit(fb, j) == kUnits) load_a1(sa, fb, j, A[fb * KS + j]);
     };
 
     // prologue: B(0), B(1) and A(0..2); wait for them, then read the first
@@ -245,13 +255,13 @@ __device__ __forceinline__ void tile_loop(const TileCtx& c, int n_pairs, uint8_t
     // three stages per iteration, so that the A ring is indexed statically
     int s = 0;
     for (; s + kRingA <= n_stages; s += kRingA) {
-        stage(s + 0, ra[0]);
-        stage(s + 1, ra[1]);
-        stage(s + 2, ra[2]);
+        stage(s + 0, ra[0], std::false_type{});
+        stage(s + 1, ra[1], std::false_type{});
+        stage(s + 2, ra[2], std::false_type{});
     }
     if (s < n_stages) {
-        stage(s, ra[0]);
-        if (s + 1 < n_stages) stage(s + 1, ra[1]);
+        stage(s, ra[0], std::true_type{});
+        if (s + 1 < n_stages) stage(s + 1, ra[1], std::true_type{});
     }
     // the last stages re-issued dummy B loads into LDS: drain them before the
     // workgroup can finish and its LDS be handed to another workgroup
