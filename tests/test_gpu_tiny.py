@@ -185,7 +185,8 @@ def test_wide_routing_layer(torch_mod, T):
 
 def _forward(torch, layer, x_t, T=None):
     T = x_t.shape[0] if T is None else T
-    y = torch.empty((T, layer.cfg.d_model), dtype=torch.int16, device="cuda")
+    # a non-zero fill, so that an output element the layer never writes shows
+    y = torch.full((T, layer.cfg.d_model), 0x3F80, dtype=torch.int16, device="cuda")
     layer.forward(0, x_t, y, T=T)
     torch.cuda.synchronize()
     return to_np_u16(y)
@@ -265,12 +266,17 @@ def _ordered(bits):
     return np.where(b & 0x8000, -mag, mag)
 
 
-def test_expert_parallel_shares(torch_mod):
+@pytest.mark.parametrize("T", [1, 2, 16])
+def test_expert_parallel_shares(torch_mod, T):
+    """Shares of 2 of the 8 experts: partial outputs (zero for tokens with no
+    local expert, and for a whole share that no token selects) summing to the
+    layer."""
     torch = torch_mod
-    wl = TINY
+    wl = TINY.with_(T=T)
     x_t, x = x_device(wl)
     full = _oracle_full(wl, x)
     total = np.zeros_like(full["y64"])
+    idle = 0
     for s in range(4):
         layer = make_layer(wl, max_tokens=wl.T, e_begin=2 * s, n_local=2)
         load_workload_host(layer, wl)
@@ -281,8 +287,11 @@ def test_expert_parallel_shares(torch_mod):
         if has.any():
             check_layer_output(y[has], ref["y64"][has])
         total += bf16_f64(y)
+        idle += not has.any()
         layer.close()
     assert rel_l2(total, full["y64"]) <= 2e-3
+    if T == 1:
+        assert idle >= 2      # top-2 of one token leaves at least two shares idle
 
 
 @pytest.mark.parametrize("T", [40, 300])
