@@ -430,12 +430,13 @@ def main():
     # Eq. (eq:pm) for the full 40-layer DBRX on 1..8 MI355X from this GPU's
     # measured streaming and matrix rates (collective latency and link
     # bandwidth are assumed: one GPU cannot measure them)
-    from paper_2506_23635_amd import perf_model
+    from paper_2506_23635_amd import perf_model, placement
     bw_meas = stack["hbm_gbs"] if stack else hbm_gbs
     tf_meas = prefill["tflops"] if prefill else MFMA_BF16_PEAK_TFLOPS * 0.4
     model = {"inputs": {"hbm_gbs_measured": bw_meas, "mfma_tflops_measured": tf_meas,
                         "collective_latency_s_assumed": 20e-6, "link_gbs_assumed": 150.0},
-             "predictions": perf_model.mi355x_predictions(bw_meas, tf_meas)}
+             "predictions": perf_model.mi355x_predictions(bw_meas, tf_meas),
+             "placements": placement.mi355x_placement_predictions(bw_meas, tf_meas)}
 
     out = {
         "metric": METRIC,
