@@ -53,10 +53,6 @@ constexpr int B_FRAGS = TB * KS;                  // 32 B fragments per stage
 constexpr int B_LOADS = B_FRAGS * 64 / kThreads;  // 8 per thread
 constexpr int B_STAGE_BYTES = B_FRAGS * kTileBytes;  // 32 KiB
 constexpr int kXcds = 8;
-#ifndef MOE_FT_BLOCK
-#define MOE_FT_BLOCK 1
-#endif
-constexpr int kFtBlock = MOE_FT_BLOCK;   // feature tiles per block of the tile order
 constexpr int kBufferFlags = 0x00020000;   // buffer descriptor word 3 (raw dword data, gfx9 family)
 constexpr int kWaitAll = (0x7 << 4) | (0xF << 8);   // vmcnt 0
 static_assert(kRingA == 3, "the K loop is unrolled by three stages");
@@ -72,19 +68,11 @@ __device__ inline f32x16_t mfma32x32x16(const u32x4_t a, const u32x4_t b, f32x16
 
 enum { kGateUp = 0, kDown = 1 };
 
-#ifndef MOE_B_SWZ
-#define MOE_B_SWZ 2
-#endif
 // chunk swizzle of B row R in LDS (a function of R mod 16 only, so 32-row
 // token blocks share it): rows 0..7 take eight distinct slots, and rows
 // 8..15 the complementary (row parity, slot) pairs, so any 8 consecutive
 // rows or 16 consecutive rows at one chunk hit distinct banks
-__device__ __forceinline__ int b_swizzle(int R)
-{
-    if (MOE_B_SWZ == 0) return R & 7;
-    if (MOE_B_SWZ == 1) return (R >> 1) & 7;
-    return (R & 7) ^ ((R >> 3) & 1);
-}
+__device__ __forceinline__ int b_swizzle(int R) { return (R & 7) ^ ((R >> 3) & 1); }
 
 struct TileCtx {
     __amdgpu_buffer_rsrc_t a_rsrc;  // buffer over the expert's packed slab (GU or DN)
@@ -395,17 +383,17 @@ __global__ __launch_bounds__(kThreads) void gemm_kernel(GemmArgs a)
     __shared__ __attribute__((aligned(16))) uint8_t lds[kRingB * B_STAGE_BYTES];
     const int M = kMode == kGateUp ? 2 * a.f : a.d;
     const int n_ftiles = (M + BM - 1) / BM;
-    // XCD-aware numbering: hardware hands block b to XCD b % 8; give each XCD
-    // a contiguous run of logical tiles.  Logical tiles walk blocks of
-    // kFtBlock feature tiles: within a block, feature tile fastest, then
-    // token tile, so the workgroups running together on one XCD share both
-    // token tiles (B) and the weight slabs of their experts (A) in its L2.
+    // XCD-aware numbering: hardware hands block b to XCD b % 8; each XCD
+    // gets a contiguous run of logical tiles (feature tile major, token tile
+    // fastest over the max_tiles slots the grid is sized for), so the
+    // workgroups running together on an XCD work on consecutive token tiles
+    // of one feature slab and share the weight slabs of their experts (A) in
+    // its L2.  Slots past the routing's token tiles exit at once.  (Splitting
+    // only the live tiles evenly over the XCDs measured no better: the XCDs'
+    // finish times differ by the mix of full and partial tiles they get.)
     const int per_xcd = gridDim.x / kXcds;
     const int logical = (blockIdx.x % kXcds) * per_xcd + blockIdx.x / kXcds;
-    const int blk = logical / (a.max_tiles * kFtBlock);
-    const int rem = logical % (a.max_tiles * kFtBlock);
-    const int tt = rem / kFtBlock;
-    const int ft = blk * kFtBlock + rem % kFtBlock;
+    const int ft = logical / a.max_tiles, tt = logical % a.max_tiles;
     if (ft >= n_ftiles || tt >= *a.n_tiles) return;
     process_tile<kMode>(a, ft, tt, lds);
 }
@@ -418,8 +406,7 @@ template <int kMode>
 static hipError_t launch_gemm(const moe::GemmArgs* a, hipStream_t s)
 {
     const int M = kMode == moe::kGateUp ? 2 * a->f : a->d;
-    const int n_blocks = ((M + moe::BM - 1) / moe::BM + moe::kFtBlock - 1) / moe::kFtBlock;
-    const int n = n_blocks * moe::kFtBlock * a->max_tiles;
+    const int n = (M + moe::BM - 1) / moe::BM * a->max_tiles;
     const int grid = (n + moe::kXcds - 1) / moe::kXcds * moe::kXcds;
     hipLaunchKernelGGL((moe::gemm_kernel<kMode>), dim3(grid), dim3(moe::kThreads), 0, s, *a);
     return hipGetLastError();
