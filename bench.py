@@ -269,6 +269,29 @@ def stack_section(steps, warmup):
     return out
 
 
+def stream_read_gbs(nbytes=4 << 30, reps=20):
+    """GB/s of the library's plain streaming read (moe_diag_stream_read) over
+    a 4 GiB buffer, far past the 256 MB last-level cache: the achievable HBM
+    read rate, reported beside the 8 TB/s spec peak."""
+    import torch
+    import paper_2506_23635_amd as moe
+    buf = torch.empty(nbytes, dtype=torch.uint8, device="cuda")
+    out = torch.zeros(4 * moe.DIAG_MAX_WG, dtype=torch.int32, device="cuda")
+    s = torch.cuda.current_stream().cuda_stream
+    for _ in range(3):
+        moe.moe_diag_stream_read(buf.data_ptr(), nbytes, out.data_ptr(), s)
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(reps):
+        moe.moe_diag_stream_read(buf.data_ptr(), nbytes, out.data_ptr(), s)
+    e1.record()
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / reps
+    del buf, out
+    torch.cuda.empty_cache()
+    return nbytes / (ms * 1e-3) / 1e9
+
+
 def measured_traffic(kernel="decode_gateup", source="moe_decode.hip"):
     """HBM bytes per launch of the dominant kernel from the committed counter
     summary (raw fabric read/write requests), or None when the kernel source
@@ -365,6 +388,10 @@ def main():
         player.close()
         return
 
+    log("timing the plain streaming read (4 GiB) ...")
+    read_gbs = stream_read_gbs()
+    log(f"streaming read {read_gbs:.0f} GB/s")
+
     wl = mi.WORKLOADS["decode"]
     log("setup decode layer (16 experts, 6.3 GB) ...")
     layer, x = setup_layer(wl, max_tokens=wl.T)
@@ -456,6 +483,8 @@ def main():
         "us_per_layer": us,
         "hbm_gbs": hbm_gbs,
         "hbm_frac": hbm_gbs / HBM_PEAK_GBS,
+        "hbm_read_ceiling_gbs": read_gbs,
+        "hbm_frac_of_ceiling": hbm_gbs / read_gbs,
         "touched_experts": touched,
         "roofline": {"bound": "hbm", "kernel": "decode_gateup", "achieved": gu_gbs,
                      "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": gu_gbs / HBM_PEAK_GBS,

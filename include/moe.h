@@ -207,6 +207,20 @@ MOE_API const char *moe_last_error(const moe_ctx *ctx);
 /* Static name of a status code. */
 MOE_API const char *moe_status_string(moe_status s);
 
+/* Diagnostics, beside the layer: one plain streaming read of `bytes` bytes of
+ * device memory at src, every 16-byte word loaded once (nontemporal, 1 KiB
+ * contiguous per wave-load, the decode GEMVs' pattern), to measure the HBM
+ * read rate the layer's weight streams can reach on this device.  So that no
+ * load is dead, workgroup b (of at most MOE_DIAG_MAX_WG) writes the XOR of
+ * the words it read to out[4b .. 4b+3] (device, MOE_DIAG_MAX_WG x 4 uint32,
+ * zeroed by the caller: the XOR of all of out is then the buffer's XOR).
+ * Enqueued on stream; allocates nothing.  src and out 16-byte aligned and
+ * bytes a multiple of 16, else MOE_E_ARG (nothing enqueued); bytes == 0
+ * enqueues nothing. */
+#define MOE_DIAG_MAX_WG 2048
+MOE_API moe_status moe_diag_stream_read(const void *src, uint64_t bytes, uint32_t *out,
+                                        moe_stream_t stream);
+
 #ifdef __cplusplus
 }
 #endif

@@ -16,13 +16,14 @@ PKG_DIR = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(PKG_DIR, "libmoe.so")
 
 MOE_OK = 0
+DIAG_MAX_WG = 2048   # MOE_DIAG_MAX_WG of include/moe.h
 STATUS_NAMES = {0: "MOE_OK", -1: "MOE_E_ARG", -2: "MOE_E_SHAPE", -3: "MOE_E_ALIGN",
                 -4: "MOE_E_CAPACITY", -5: "MOE_E_STATE", -6: "MOE_E_HIP"}
 
 EXPORTED = ["moe_weight_bytes", "moe_workspace_bytes", "moe_init", "moe_load_expert",
             "moe_load_router", "moe_route", "moe_forward", "moe_forward_stack",
             "moe_intermediates", "moe_profile_enable", "moe_profile_read", "moe_destroy",
-            "moe_last_error", "moe_status_string"]
+            "moe_last_error", "moe_status_string", "moe_diag_stream_read"]
 
 KERNEL_KINDS = ["router", "route", "decode_gateup", "decode_down", "gemm_gateup", "gemm_down",
                 "combine", "pack"]
@@ -84,9 +85,10 @@ def lib():
         L.moe_last_error.restype = ctypes.c_char_p
         L.moe_status_string.argtypes = [ctypes.c_int]
         L.moe_status_string.restype = ctypes.c_char_p
+        L.moe_diag_stream_read.argtypes = [P, ctypes.c_uint64, P, P]
         for fn in ("moe_init", "moe_load_expert", "moe_load_router", "moe_route", "moe_forward",
                    "moe_forward_stack", "moe_intermediates", "moe_profile_enable",
-                   "moe_profile_read"):
+                   "moe_profile_read", "moe_diag_stream_read"):
             getattr(L, fn).restype = ctypes.c_int
         _lib = L
     return _lib
@@ -140,6 +142,15 @@ def moe_forward(ctx, layer, x_ptr, T, routing, y_ptr, stream=0):
 
 def moe_forward_stack(ctx, x_ptr, T, stream=0):
     _check(ctx, lib().moe_forward_stack(ctx, x_ptr, T, stream))
+
+
+def moe_diag_stream_read(src_ptr, nbytes, out_ptr, stream=0):
+    """One plain streaming read of nbytes at src_ptr; workgroup b writes the
+    XOR of its words to the 4 uint32 at out_ptr + 16 b (device pointers; out
+    holds DIAG_MAX_WG x 4 uint32, zeroed by the caller; see include/moe.h)."""
+    st = lib().moe_diag_stream_read(src_ptr, nbytes, out_ptr, stream)
+    if st != MOE_OK:
+        raise MoeError(st, lib().moe_status_string(st).decode())
 
 
 def moe_intermediates(ctx):

@@ -134,3 +134,15 @@ def test_status_strings():
     L = moe.lib()
     assert L.moe_status_string(0) == b"MOE_OK"
     assert L.moe_status_string(-4) == b"MOE_E_CAPACITY"
+
+
+def test_diag_stream_read_rejects_bad_arguments():
+    # argument checks run before any launch (no GPU needed)
+    lib = moe.lib()
+    aligned = 1 << 20
+    assert lib.moe_diag_stream_read(None, 16, aligned, None) == E_ARG
+    assert lib.moe_diag_stream_read(aligned, 16, None, None) == E_ARG
+    assert lib.moe_diag_stream_read(aligned + 8, 16, aligned, None) == E_ARG
+    assert lib.moe_diag_stream_read(aligned, 17, aligned, None) == E_ARG
+    assert lib.moe_diag_stream_read(aligned, 16, aligned + 4, None) == E_ARG
+    assert lib.moe_diag_stream_read(aligned, 0, aligned, None) == moe.MOE_OK

@@ -362,3 +362,23 @@ def test_stack_three_layers(torch_mod):
         cur = oracle.residual_add(cur, ref["y"])
     assert rel_l2(bf16_f64(got), bf16_f64(cur)) <= 2e-3
     layer.close()
+
+
+@pytest.mark.parametrize("nbytes", [16, (1 << 20) + 48, (200 << 20) + 16])
+def test_diag_stream_read_reads_every_word_once(torch_mod, nbytes):
+    """The bench's streaming-read ceiling: the XOR of the per-workgroup XORs
+    equals the XOR of the buffer's 16-byte words (each read once), for sizes
+    from one workgroup to a partial last chunk and the unrolled loop's
+    remainder."""
+    import paper_2506_23635_amd as moe
+    torch = torch_mod
+    g = torch.Generator(device="cuda").manual_seed(5)
+    buf = torch.randint(-2**31, 2**31 - 1, (nbytes // 4,), dtype=torch.int32, device="cuda", generator=g)
+    out = torch.zeros(4 * moe.DIAG_MAX_WG, dtype=torch.int32, device="cuda")
+    moe.moe_diag_stream_read(buf.data_ptr(), nbytes, out.data_ptr(),
+                             torch.cuda.current_stream().cuda_stream)
+    torch.cuda.synchronize()
+    words = buf.cpu().numpy().view(np.uint32).reshape(-1, 4)
+    expect = np.bitwise_xor.reduce(words, axis=0)
+    got = np.bitwise_xor.reduce(out.cpu().numpy().view(np.uint32).reshape(-1, 4), axis=0)
+    assert np.array_equal(got, expect)
