@@ -23,7 +23,7 @@
  *     unselected ones in the weighted sum gives the same result; that dense
  *     form is oracle_layer_dense() below.
  *
- * Readings where the paper is silent (each is listed in the design doc):
+ * Readings where the paper is silent (R1..R8):
  *   R1 router = one linear map, fp32 weights [d,E]; logit = fp32 rounding of
  *      the exact dot product, then an optional fp32 bias is added in fp32.
  *   R2 selection by logit, ties to the lower expert id, slots ordered by
