@@ -191,7 +191,9 @@ class MoeLayer:
     Only allocation and pointer marshalling happen here; all compute is in
     the library."""
 
-    def __init__(self, cfg: MoeConfig, device="cuda"):
+    def __init__(self, cfg: MoeConfig, device="cuda", arena=None, workspace=None):
+        """arena / workspace: caller-owned uint8 device tensors of at least
+        moe_weight_bytes / moe_workspace_bytes (allocated here if None)."""
         import torch
         self.torch = torch
         self.cfg = cfg
@@ -200,8 +202,11 @@ class MoeLayer:
         sb = moe_workspace_bytes(cfg)
         if wb == 0 or sb == 0:
             raise MoeError(-2, "invalid config")
-        self.arena = torch.empty(wb, dtype=torch.uint8, device=self.device)
-        self.workspace = torch.empty(sb, dtype=torch.uint8, device=self.device)
+        if arena is not None and arena.numel() < wb or workspace is not None and workspace.numel() < sb:
+            raise MoeError(-1, "arena or workspace smaller than the config needs")
+        self.arena = torch.empty(wb, dtype=torch.uint8, device=self.device) if arena is None else arena
+        self.workspace = (torch.empty(sb, dtype=torch.uint8, device=self.device)
+                          if workspace is None else workspace)
         self.ctx = moe_init(cfg, self.arena.data_ptr(), self.workspace.data_ptr())
 
     @property
