@@ -3,6 +3,7 @@ library routines, brute force, closed forms, invariants and special cases.
 None of these use the GPU library."""
 import itertools
 import math
+import os
 from fractions import Fraction
 
 import numpy as np
@@ -408,3 +409,32 @@ def test_residual_add_brute_force():
         s = float(mi.bf16_bits_to_f32(x[i:i + 1])[0]) + float(mi.bf16_bits_to_f32(y[i:i + 1])[0])
         assert got[i] == _nearest_even_bf16(s) or (s == 0.0 and (got[i] & 0x7FFF) == 0)
     assert rng is not None
+
+
+def test_bf16_from_f64_matches_torch_on_every_fp32_pattern():
+    """Exhaustive: for all 2^32 fp32 bit patterns, the oracle's double->bf16
+    (every fp32 value is exact in fp64) equals torch's fp32->bf16
+    round-to-nearest-even; NaN stays NaN."""
+    from concurrent.futures import ThreadPoolExecutor
+    chunk = 1 << 24
+    base = np.arange(chunk, dtype=np.uint32)
+
+    def check(start):
+        f = (base + np.uint32(start)).view(np.float32)
+        want = torch.from_numpy(f).to(torch.bfloat16).view(torch.int16).numpy().view(np.uint16)
+        with np.errstate(invalid="ignore"):
+            got = oracle.bf16_round(f.astype(np.float64))
+        nan = np.isnan(f)
+        if not nan.any():
+            return bool(np.array_equal(got, want))
+        return bool(np.array_equal(got[~nan], want[~nan]) and
+                    np.all(np.isnan(mi.bf16_bits_to_f32(got[nan]))))
+
+    torch.set_num_threads(1)
+    try:
+        with ThreadPoolExecutor(min(8, os.cpu_count() or 1)) as ex:
+            bad = [hex(s) for s, ok in zip(range(0, 1 << 32, chunk),
+                                           ex.map(check, range(0, 1 << 32, chunk))) if not ok]
+    finally:
+        torch.set_num_threads(os.cpu_count() or 1)
+    assert not bad, bad[:8]
