@@ -170,6 +170,76 @@ def test_prefill_layer_sampled_tokens(torch_mod, prefill_layer, prefill_ref):
     assert np.all(np.isfinite(bf16_f64(y)))
 
 
+def _edge_rows(r0, r1, tile=256):
+    """Grouped rows of one expert at MFMA-block (32), pair (64) and tile
+    (256) edges, and its last row (the partial tile's end)."""
+    out = set()
+    for base in range(r0, r1, tile):
+        for off in (0, 31, 32, 63, 64, 127, 128, 191, 192, tile - 1):
+            if base + off < r1:
+                out.add(base + off)
+    out.add(r1 - 1)
+    return sorted(out)
+
+
+def test_prefill_tile_edges(torch_mod, prefill_layer, prefill_ref):
+    """Full DBRX shape, 2048 skewed tokens: for every expert, the grouped rows
+    at block, pair and tile edges and the last row of its partial tile.  H
+    against the oracle within the fp32-accumulation bound (and mostly
+    bit-exact); O against an fp64 down projection of the GPU's own H within
+    gamma_f * sum |h||w2|; y of the rows' tokens against the oracle."""
+    import paper_2506_23635_amd as moe
+    torch = torch_mod
+    x, lg, idx, w = prefill_ref
+    x_t = torch.from_numpy(x.view(np.int16)).cuda()
+    y = run_forward(torch, prefill_layer, x_t)
+    rt = prefill_layer.routing_tensors(prefill_layer.route(0, x_t))   # same routing
+    hptr, optr = moe.moe_intermediates(prefill_layer.ctx)
+    rows, d, f = int(rt["offsets"][-1]), PREFILL.d, PREFILL.f
+    H = torch.empty((rows, f), dtype=torch.int16, device="cuda")
+    O = torch.empty((rows, d), dtype=torch.float32, device="cuda")
+    moe._copy_dev(H.data_ptr(), hptr, H.numel() * 2)
+    moe._copy_dev(O.data_ptr(), optr, O.numel() * 4)
+    torch.cuda.synchronize()
+    H = H.cpu().numpy().view(np.uint16)
+    O = O.cpu().numpy().astype(np.float64)
+    u32 = 2.0 ** -24
+    gd, gf = d * u32 / (1 - d * u32), f * u32 / (1 - f * u32)
+    tokens, exact, checked = set(), [], 0
+    for e in range(PREFILL.E):
+        r0, r1 = int(rt["offsets"][e]), int(rt["offsets"][e + 1])
+        if r1 == r0:
+            continue
+        er = _edge_rows(r0, r1)
+        toks = rt["row_token"][er]
+        tokens.update(toks.tolist())
+        g_w, u_w, d_w = host_weights(PREFILL, e)
+        hb, _ = oracle.expert_glu(x[toks], g_w, u_w, d_w)
+        xf, w1, v1 = bf16_f64(x[toks]), bf16_f64(g_w), bf16_f64(u_w)
+        g, u = xf @ w1, xf @ v1
+        s1, s2 = np.abs(xf) @ np.abs(w1), np.abs(xf) @ np.abs(v1)
+        sig = 1.0 / (1.0 + np.exp(-g))
+        silu, dsilu = g * sig, sig * (1.0 + g * (1.0 - sig))
+        ref = bf16_f64(hb)
+        step = np.spacing(np.abs(ref).astype(np.float32)).astype(np.float64) * 65536.0
+        bound = step + gd * (np.abs(dsilu * u) * s1 + np.abs(silu) * s2) + 8 * u32 * np.abs(silu * u)
+        hg = bf16_f64(H[er])
+        assert np.all(np.abs(hg - ref) <= bound), (e, float((np.abs(hg - ref) / bound).max()))
+        exact.append(np.mean(hg == ref))
+        # down projection of the GPU's own H: bf16 x bf16 products are exact in
+        # fp32, so only the accumulation rounds
+        w2 = bf16_f64(d_w)
+        o_ref = hg @ w2
+        o_bound = gf * (np.abs(hg) @ np.abs(w2)) + 1e-30
+        assert np.all(np.abs(O[er] - o_ref) <= o_bound), (e, float((np.abs(O[er] - o_ref) / o_bound).max()))
+        checked += len(er)
+    assert checked > 100 and np.mean(exact) > 0.9
+    picks = sorted(tokens)
+    G, U, D = weights_for(PREFILL, range(PREFILL.E))
+    y64, _ = oracle.layer_with_routing(x[picks], idx[picks], w[picks], G, U, D)
+    check_layer_output(y[picks], y64)
+
+
 def test_prefill_deterministic(torch_mod, prefill_layer, prefill_ref):
     torch = torch_mod
     x = prefill_ref[0]
