@@ -80,6 +80,10 @@ def test_decode_full_layer(torch_mod, decode_layer, T):
     G, U, D = weights_for(wl, sorted(set(idx.reshape(-1).tolist())))
     y64, _ = oracle.layer_with_routing(x, idx, w, G, U, D)
     check_layer_output(y, y64)
+    # the K-split GEMVs' H and O, every row
+    checked, exact, _ = check_intermediates(torch, decode_layer, wl, x, rt,
+                                            lambda r0, r1: list(range(r0, r1)))
+    assert checked == T * wl.k and exact > 0.9
 
 
 @pytest.mark.parametrize("T", [1, 4, 8])
@@ -182,20 +186,17 @@ def _edge_rows(r0, r1, tile=256):
     return sorted(out)
 
 
-def test_prefill_tile_edges(torch_mod, prefill_layer, prefill_ref):
-    """Full DBRX shape, 2048 skewed tokens: for every expert, the grouped rows
-    at block, pair and tile edges and the last row of its partial tile.  H
-    against the oracle within the fp32-accumulation bound (and mostly
-    bit-exact); O against an fp64 down projection of the GPU's own H within
-    gamma_f * sum |h||w2|; y of the rows' tokens against the oracle."""
+def check_intermediates(torch, layer, wl, x, rt, pick_rows):
+    """H and O of the layer's last forward, for the grouped rows
+    pick_rows(r0, r1) of every expert: H against the oracle within the
+    fp32-accumulation bound (gamma_d sum |x||w| carried through silu(g) u,
+    one bf16 step, a few fp32 ulps for the logistic); O against an fp64 down
+    projection of the GPU's own H within gamma_f sum |h||w2| (bf16 x bf16
+    products are exact in fp32, so only the accumulation rounds).  Returns
+    (rows checked, fraction of H bit-exact, tokens of the checked rows)."""
     import paper_2506_23635_amd as moe
-    torch = torch_mod
-    x, lg, idx, w = prefill_ref
-    x_t = torch.from_numpy(x.view(np.int16)).cuda()
-    y = run_forward(torch, prefill_layer, x_t)
-    rt = prefill_layer.routing_tensors(prefill_layer.route(0, x_t))   # same routing
-    hptr, optr = moe.moe_intermediates(prefill_layer.ctx)
-    rows, d, f = int(rt["offsets"][-1]), PREFILL.d, PREFILL.f
+    hptr, optr = moe.moe_intermediates(layer.ctx)
+    rows, d, f = int(rt["offsets"][-1]), wl.d, wl.f
     H = torch.empty((rows, f), dtype=torch.int16, device="cuda")
     O = torch.empty((rows, d), dtype=torch.float32, device="cuda")
     moe._copy_dev(H.data_ptr(), hptr, H.numel() * 2)
@@ -206,14 +207,14 @@ def test_prefill_tile_edges(torch_mod, prefill_layer, prefill_ref):
     u32 = 2.0 ** -24
     gd, gf = d * u32 / (1 - d * u32), f * u32 / (1 - f * u32)
     tokens, exact, checked = set(), [], 0
-    for e in range(PREFILL.E):
+    for e in range(wl.E):
         r0, r1 = int(rt["offsets"][e]), int(rt["offsets"][e + 1])
         if r1 == r0:
             continue
-        er = _edge_rows(r0, r1)
+        er = pick_rows(r0, r1)
         toks = rt["row_token"][er]
         tokens.update(toks.tolist())
-        g_w, u_w, d_w = host_weights(PREFILL, e)
+        g_w, u_w, d_w = host_weights(wl, e)
         hb, _ = oracle.expert_glu(x[toks], g_w, u_w, d_w)
         xf, w1, v1 = bf16_f64(x[toks]), bf16_f64(g_w), bf16_f64(u_w)
         g, u = xf @ w1, xf @ v1
@@ -226,15 +227,26 @@ def test_prefill_tile_edges(torch_mod, prefill_layer, prefill_ref):
         hg = bf16_f64(H[er])
         assert np.all(np.abs(hg - ref) <= bound), (e, float((np.abs(hg - ref) / bound).max()))
         exact.append(np.mean(hg == ref))
-        # down projection of the GPU's own H: bf16 x bf16 products are exact in
-        # fp32, so only the accumulation rounds
         w2 = bf16_f64(d_w)
         o_ref = hg @ w2
         o_bound = gf * (np.abs(hg) @ np.abs(w2)) + 1e-30
         assert np.all(np.abs(O[er] - o_ref) <= o_bound), (e, float((np.abs(O[er] - o_ref) / o_bound).max()))
         checked += len(er)
-    assert checked > 100 and np.mean(exact) > 0.9
-    picks = sorted(tokens)
+    return checked, float(np.mean(exact)), sorted(tokens)
+
+
+def test_prefill_tile_edges(torch_mod, prefill_layer, prefill_ref):
+    """Full DBRX shape, 2048 skewed tokens: for every expert, the grouped rows
+    at block, pair and tile edges and the last row of its partial tile; H and
+    O (check_intermediates), and y of those rows' tokens against the
+    oracle."""
+    torch = torch_mod
+    x, lg, idx, w = prefill_ref
+    x_t = torch.from_numpy(x.view(np.int16)).cuda()
+    y = run_forward(torch, prefill_layer, x_t)
+    rt = prefill_layer.routing_tensors(prefill_layer.route(0, x_t))   # same routing
+    checked, exact, picks = check_intermediates(torch, prefill_layer, PREFILL, x, rt, _edge_rows)
+    assert checked > 100 and exact > 0.9
     G, U, D = weights_for(PREFILL, range(PREFILL.E))
     y64, _ = oracle.layer_with_routing(x[picks], idx[picks], w[picks], G, U, D)
     check_layer_output(y[picks], y64)
