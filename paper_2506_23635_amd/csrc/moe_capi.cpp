@@ -30,7 +30,7 @@ struct Layout {
     size_t router_bytes, bias_off, gu_bytes, dn_bytes, expert_bytes, experts_off, layer_bytes;
     size_t arena_bytes;
     // workspace
-    size_t dpart_off, counter_off, logits_off, idx_off, w_off, counts_off, offsets_off, pair_row_off,
+    size_t dpart_off, logits_off, idx_off, w_off, counts_off, offsets_off, pair_row_off,
         row_token_off, active_off, tiles_off, n_tiles_off, h_off, o_off, ws_bytes;
     int rows_max, max_tiles;
 };
@@ -76,7 +76,6 @@ Layout make_layout(const moe_config* c)
     size_t off = 0;
     auto take = [&](size_t bytes) { size_t o = off; off = align_up(off + bytes, kAlign); return o; };
     L.dpart_off = take((size_t)moe_route_decode_wgs(c->d_model) * 16 * 16 * 8);
-    L.counter_off = take(4);
     L.logits_off = take(Tm * E * 4);
     L.idx_off = take(Tm * k * 4);
     L.w_off = take(Tm * k * 4);
@@ -107,7 +106,6 @@ struct moe_ctx {
     std::vector<uint8_t> expert_loaded;   // [n_layers * n_local]
     moe::RouteView rv;
     bool gemm_lds_set;      // dynamic-LDS limit raised for the GEMM kernels
-    bool counter_ready;     // decode-route ticket counter zeroed on this workspace
     // per-kernel timing (moe_profile_*): an event pair around each launch
     bool prof_on;
     std::vector<hipEvent_t> prof_events;   // 2 per launch slot
@@ -179,15 +177,9 @@ moe_status do_route(moe_ctx* ctx, int layer, const uint16_t* x, int T, const flo
     const int tile_rows = moe_prefill_tile_rows();
     hipError_t e;
     if (!logits_in && moe_route_decode_ok(T, c.n_experts, c.top_k)) {
-        unsigned int* counter = reinterpret_cast<unsigned int*>(ctx->ws + ctx->L.counter_off);
-        if (!ctx->counter_ready) {
-            e = moe_launch_zero_counter(counter, s);
-            if (e != hipSuccess) return hip_fail(ctx, e, "counter init launch");
-            ctx->counter_ready = true;
-        }
         double* dpart = reinterpret_cast<double*>(ctx->ws + ctx->L.dpart_off);
         e = timed(ctx, MOE_K_ROUTE, s, [&] {
-            return moe_launch_route_decode(x, wrT, bias, dpart, counter, T, c.d_model, c.n_experts,
+            return moe_launch_route_decode(x, wrT, bias, dpart, T, c.d_model, c.n_experts,
                                            c.top_k, c.expert_begin, c.n_local_experts, tile_rows,
                                            &ctx->rv, s);
         });
@@ -346,7 +338,6 @@ moe_status moe_init(const moe_config* cfg, void* weight_arena, void* workspace, 
     c->rv.n_tiles = reinterpret_cast<int32_t*>(w + c->L.n_tiles_off);
     c->route_valid = false;
     c->gemm_lds_set = false;
-    c->counter_ready = false;
     c->prof_on = false;
     c->prof_dropped = 0;
     *out = c;

@@ -151,10 +151,9 @@ hipError_t moe_launch_pack(const uint16_t* src, int K, int N, void* dst, int rt_
                            hipStream_t s);
 int moe_route_decode_ok(int T, int E, int k);
 int moe_route_decode_wgs(int d);
-hipError_t moe_launch_zero_counter(unsigned int* counter, hipStream_t s);
 hipError_t moe_launch_route_decode(const uint16_t* x, const float* wrT, const float* bias,
-                                   double* partial, unsigned int* counter, int T, int d, int E,
-                                   int k, int e_begin, int n_local, int tile_rows,
+                                   double* partial, int T, int d, int E, int k, int e_begin,
+                                   int n_local, int tile_rows,
                                    const moe::RouteView* rv, hipStream_t s);
 hipError_t moe_launch_router_select(const uint16_t* x, const float* wrT, const float* bias, int T,
                                    int d, int E, int k, const moe::RouteView* rv, hipStream_t s);

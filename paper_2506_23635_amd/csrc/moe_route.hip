@@ -104,13 +104,15 @@ __device__ inline void fma8(double& acc, const u32x4_t xv, const float4 w0, cons
 
 constexpr int kSmallT = 16;
 
-// Decode routing (T <= 16, E <= 16, T*k <= 64): the logits are spread over
-// n_wg workgroups, each owning d/n_wg of the reduction axis (8-wide groups,
-// thread = (expert tid%16, group tid/16)).  Per workgroup the
-// partials are reduced in fixed order (lane butterfly, then over the 16 waves
-// through LDS) and written to the workspace; the workgroup that takes the last
-// ticket of a device-scope counter sums the n_wg partials in workgroup order,
-// selects, weighs and permutes, and rewinds the counter for the next call.
+// Decode routing (T <= 16, E <= 16, T*k <= 64) in two launches.
+// route_partials_kernel spreads the logits over n_wg workgroups, each owning
+// d/n_wg of the reduction axis (8-wide groups, thread = (expert tid%16, group
+// tid/16)); per workgroup the partials are reduced in fixed order (lane
+// butterfly, then over the 16 waves through LDS) and written to the
+// workspace.  route_finish_kernel, one workgroup, sums the n_wg partials in
+// workgroup order, selects, weighs and permutes.  The kernel boundary orders
+// the two: measured, it costs less than a release fence, a device-scope
+// ticket and an acquire inside one launch (~9 us of a 14 us kernel).
 constexpr int kDecE = 16;
 constexpr int kDecPairs = 64;
 constexpr int kDecMaxWg = 16;   // partial sums read in one batch (d <= 8192)
@@ -120,22 +122,14 @@ struct DecodeRouteArgs {
     const float* wrT;
     const float* bias;
     double* partial;          // [n_wg][kSmallT][kDecE]
-    unsigned int* counter;    // one device-scope ticket counter (0 between calls)
     int T, d, E, k, e_begin, n_local, tile_rows, n_wg;
     RouteView rv;
 };
 
-__global__ __launch_bounds__(kRouteThreads) void route_decode_kernel(DecodeRouteArgs a)
+__global__ __launch_bounds__(kRouteThreads) void route_partials_kernel(DecodeRouteArgs a)
 {
     __shared__ double wsum[kRouteWaves][kSmallT][kDecE];
-    __shared__ float lg[kSmallT][kDecE];
-    __shared__ int s_ids[kDecPairs];
-    __shared__ float s_w[kDecPairs];
-    __shared__ int s_rank[kSmallT][kDecE];
-    __shared__ int s_cnt[kDecE];
-    __shared__ int s_off[kDecE + 1];
-    __shared__ int s_last;
-    const int T = a.T, E = a.E, d = a.d, k = a.k;
+    const int T = a.T, E = a.E, d = a.d;
     const int tid = threadIdx.x;
     const int lane = tid & 63, wid = tid >> 6;
     const int e = tid & 15;
@@ -170,16 +164,23 @@ __global__ __launch_bounds__(kRouteThreads) void route_decode_kernel(DecodeRoute
         for (int w = 0; w < kRouteWaves; ++w) v += wsum[w][t][ee];
         a.partial[((int64_t)blockIdx.x * kSmallT + t) * kDecE + ee] = v;
     }
-    __threadfence();
-    __syncthreads();
-    if (tid == 0) s_last = (atomicAdd(a.counter, 1u) == (unsigned)(a.n_wg - 1)) ? 1 : 0;
-    __syncthreads();
-    if (!s_last) return;
-    __threadfence();
-    // the last workgroup: logits, selection and permutation in LDS, then
-    // every routing output written at the end (global stores are not waited
-    // for inside the workgroup).  Every step is spread over threads: one
-    // (token, expert) pair per thread.
+}
+
+// logits, selection and permutation in LDS, then every routing output
+// written at the end (global stores are not waited for inside the
+// workgroup).  Every step is spread over threads: one (token, expert) pair
+// per thread.
+__global__ __launch_bounds__(kRouteThreads) void route_finish_kernel(DecodeRouteArgs a)
+{
+    __shared__ float lg[kSmallT][kDecE];
+    __shared__ int s_ids[kDecPairs];
+    __shared__ float s_w[kDecPairs];
+    __shared__ int s_rank[kSmallT][kDecE];
+    __shared__ int s_cnt[kDecE];
+    __shared__ int s_off[kDecE + 1];
+    const int T = a.T, E = a.E, k = a.k;
+    const int tid = threadIdx.x;
+    const int lane = tid & 63, wid = tid >> 6;
     if (tid < T * kDecE) {
         const int t = tid / kDecE, ee = tid % kDecE;
         if (ee < E) {
@@ -202,7 +203,6 @@ __global__ __launch_bounds__(kRouteThreads) void route_decode_kernel(DecodeRoute
             lg[t][ee] = l;
         }
     }
-    if (tid == 0) *a.counter = 0u;
     lds_barrier();
     // rank of expert e in its token's order (logit descending, id ascending):
     // the experts before e with a logit >= its own and those after it with a
@@ -304,8 +304,6 @@ __global__ __launch_bounds__(kRouteThreads) void route_decode_kernel(DecodeRoute
         if (ee < E) a.rv.logits[(int64_t)t * E + ee] = lg[t][ee];
     }
 }
-
-__global__ void zero_u32_kernel(unsigned int* p) { *p = 0u; }
 
 // Router and selection for many tokens: 8 tokens per 256-thread workgroup;
 // wave w takes tokens 4(w/2) .. +3 and experts 8(w%2) .. +7 (then +16, ...).
@@ -612,25 +610,22 @@ extern "C" int moe_route_decode_ok(int T, int E, int k)
 extern "C" int moe_route_decode_wgs(int d) { return (d / 8 + 63) / 64; }
 
 
-extern "C" hipError_t moe_launch_zero_counter(unsigned int* counter, hipStream_t s)
-{
-    hipLaunchKernelGGL(moe::zero_u32_kernel, dim3(1), dim3(1), 0, s, counter);
-    return hipGetLastError();
-}
 
 extern "C" hipError_t moe_launch_route_decode(const uint16_t* x, const float* wrT,
-                                              const float* bias, double* partial,
-                                              unsigned int* counter, int T, int d, int E, int k,
-                                              int e_begin, int n_local, int tile_rows,
+                                              const float* bias, double* partial, int T, int d,
+                                              int E, int k, int e_begin, int n_local, int tile_rows,
                                               const moe::RouteView* rv, hipStream_t s)
 {
     moe::DecodeRouteArgs a{};
-    a.x = x; a.wrT = wrT; a.bias = bias; a.partial = partial; a.counter = counter;
+    a.x = x; a.wrT = wrT; a.bias = bias; a.partial = partial;
     a.T = T; a.d = d; a.E = E; a.k = k;
     a.e_begin = e_begin; a.n_local = n_local; a.tile_rows = tile_rows;
     a.rv = *rv;
     a.n_wg = moe_route_decode_wgs(d);
-    hipLaunchKernelGGL(moe::route_decode_kernel, dim3(a.n_wg), dim3(moe::kRouteThreads), 0, s, a);
+    hipLaunchKernelGGL(moe::route_partials_kernel, dim3(a.n_wg), dim3(moe::kRouteThreads), 0, s, a);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL(moe::route_finish_kernel, dim3(1), dim3(moe::kRouteThreads), 0, s, a);
     return hipGetLastError();
 }
 
