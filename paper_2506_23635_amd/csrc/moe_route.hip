@@ -13,8 +13,9 @@
 //   router_select_kernel: 8 tokens per workgroup, a wave takes 4 tokens x 8
 //       experts, each dot product split over the 64 lanes and summed by a
 //       fixed transpose-reduce; then each token's selection.
-//   route_decode_kernel (T <= 16, E <= 16, T*k <= 64): the logits spread over
-//       d/512 workgroups, the last one to finish selects and permutes.
+//   route_partials_kernel + route_finish_kernel (T <= 16, E <= 16,
+//       T*k <= 64): partial logits over a few workgroups, then one workgroup
+//       sums them in fixed order, selects and permutes.
 //   select_kernel: selection and weights from caller-supplied fp32 logits.
 //   permute_kernel: the permutation and the GEMM tile list (one workgroup).
 //
