@@ -331,7 +331,7 @@ def cpu_baseline(wl, budget_s=10.0):
         oracle.layer(x, wr, wl.bias(), G, U, D, wl.k)
         reps += 1
         el = time.perf_counter() - t0
-        if el >= budget_s or reps >= 50:
+        if el >= budget_s or reps >= 1000:
             break
     threads = int(os.environ.get("OMP_NUM_THREADS", "0") or 0) or os.cpu_count()
     assert np.isfinite(el)

@@ -185,6 +185,27 @@ def moe_last_error(ctx) -> str:
 
 # ------------------------------------------------------------ torch helper --
 
+def _tensor_ptr(t, name, min_numel, dtypes, device):
+    """Checks a torch tensor before its address crosses the C-ABI, which
+    cannot see sizes: one of `dtypes`, contiguous, on `device` (None: any),
+    at least `min_numel` elements.  Returns its data pointer."""
+    if t is None:
+        raise MoeError(-1, f"{name} is None")
+    if t.dtype not in dtypes:
+        raise MoeError(-1, f"{name} has dtype {t.dtype}, expected one of {list(dtypes)}")
+    if not t.is_contiguous():
+        raise MoeError(-1, f"{name} must be contiguous")
+    if device is not None and t.device != device:
+        raise MoeError(-1, f"{name} is on {t.device}, expected {device}")
+    if t.numel() < min_numel:
+        raise MoeError(-2, f"{name} has {t.numel()} elements, the call uses {min_numel}")
+    return t.data_ptr()
+
+
+def _bf16_types(torch):
+    # bf16 tensors may arrive as bfloat16 or as their 16-bit integer bits
+    return (torch.bfloat16, torch.int16, torch.uint16)
+
 class MoeLayer:
     """Owns a context plus its torch-allocated arena and workspace on one GPU.
 
@@ -198,6 +219,10 @@ class MoeLayer:
         self.torch = torch
         self.cfg = cfg
         self.device = torch.device(device)
+        if self.device.type != "cuda":
+            raise MoeError(-1, f"the layer runs on a GPU, not on {self.device}")
+        if self.device.index is None:
+            self.device = torch.device("cuda", torch.cuda.current_device())
         wb = moe_weight_bytes(cfg)
         sb = moe_workspace_bytes(cfg)
         if wb == 0 or sb == 0:
@@ -207,7 +232,8 @@ class MoeLayer:
         self.arena = torch.empty(wb, dtype=torch.uint8, device=self.device) if arena is None else arena
         self.workspace = (torch.empty(sb, dtype=torch.uint8, device=self.device)
                           if workspace is None else workspace)
-        self.ctx = moe_init(cfg, self.arena.data_ptr(), self.workspace.data_ptr())
+        self.ctx = moe_init(cfg, _tensor_ptr(self.arena, "arena", wb, (torch.uint8,), self.device),
+                            _tensor_ptr(self.workspace, "workspace", sb, (torch.uint8,), self.device))
 
     @property
     def stream(self) -> int:
@@ -224,29 +250,57 @@ class MoeLayer:
         except Exception:
             pass
 
-    # tensors are torch tensors on self.device (bf16 as int16/uint16 views)
+    # Tensors: row-major, contiguous; bf16 as bfloat16 or int16/uint16 bits;
+    # activations on self.device, weights on self.device or all on the host.
+    # Every tensor is checked (dtype, layout, device, element count) before
+    # its address is handed to the library.
+    def _src_device(self, *ts):
+        on_dev = ts[0].is_cuda
+        if any(t is not None and t.is_cuda != on_dev for t in ts):
+            raise MoeError(-1, "weights must be all on the GPU or all on the host")
+        return on_dev, (self.device if on_dev else self.torch.device("cpu"))
+
     def load_expert(self, layer, expert, gate, up, down):
-        on_dev = int(gate.is_cuda)
-        moe_load_expert(self.ctx, layer, expert, gate.data_ptr(), up.data_ptr(), down.data_ptr(),
-                        on_dev, self.stream if on_dev else 0)
+        c, bf = self.cfg, _bf16_types(self.torch)
+        on_dev, dev = self._src_device(gate, up, down)
+        n = c.d_model * c.ffn_dim
+        moe_load_expert(self.ctx, layer, expert, _tensor_ptr(gate, "gate", n, bf, dev),
+                        _tensor_ptr(up, "up", n, bf, dev), _tensor_ptr(down, "down", n, bf, dev),
+                        int(on_dev), self.stream if on_dev else 0)
 
     def load_router(self, layer, wr, bias=None):
-        on_dev = int(wr.is_cuda)
-        moe_load_router(self.ctx, layer, wr.data_ptr(), bias.data_ptr() if bias is not None else None,
-                        on_dev, self.stream if on_dev else 0)
+        c, f32 = self.cfg, (self.torch.float32,)
+        on_dev, dev = self._src_device(wr, bias)
+        moe_load_router(self.ctx, layer, _tensor_ptr(wr, "wr", c.d_model * c.n_experts, f32, dev),
+                        _tensor_ptr(bias, "bias", c.n_experts, f32, dev) if bias is not None else None,
+                        int(on_dev), self.stream if on_dev else 0)
+
+    def _tokens(self, x, T):
+        T = x.shape[0] if T is None else int(T)
+        if T < 0:
+            raise MoeError(-1, "T is negative")
+        return T
 
     def route(self, layer, x, T=None, logits_in=None) -> MoeRouting:
-        T = x.shape[0] if T is None else T
-        return moe_route(self.ctx, layer, x.data_ptr() if x is not None else None, T,
-                         logits_in.data_ptr() if logits_in is not None else None, self.stream)
+        if x is None and logits_in is None:
+            raise MoeError(-1, "route needs x or logits_in")
+        T = self._tokens(x if x is not None else logits_in, T)
+        d, E = self.cfg.d_model, self.cfg.n_experts
+        xp = _tensor_ptr(x, "x", T * d, _bf16_types(self.torch), self.device) if x is not None else None
+        lp = (_tensor_ptr(logits_in, "logits_in", T * E, (self.torch.float32,), self.device)
+              if logits_in is not None else None)
+        return moe_route(self.ctx, layer, xp, T, lp, self.stream)
 
     def forward(self, layer, x, y, routing=None, T=None):
-        T = x.shape[0] if T is None else T
-        moe_forward(self.ctx, layer, x.data_ptr(), T, routing, y.data_ptr(), self.stream)
+        T = self._tokens(x, T)
+        n, bf = T * self.cfg.d_model, _bf16_types(self.torch)
+        moe_forward(self.ctx, layer, _tensor_ptr(x, "x", n, bf, self.device), T, routing,
+                    _tensor_ptr(y, "y", n, bf, self.device), self.stream)
 
     def forward_stack(self, x, T=None):
-        T = x.shape[0] if T is None else T
-        moe_forward_stack(self.ctx, x.data_ptr(), T, self.stream)
+        T = self._tokens(x, T)
+        moe_forward_stack(self.ctx, _tensor_ptr(x, "x", T * self.cfg.d_model, _bf16_types(self.torch),
+                                                self.device), T, self.stream)
 
     def routing_tensors(self, r: MoeRouting):
         """Copies the routing views (device) to host numpy arrays."""

@@ -146,3 +146,38 @@ def test_diag_stream_read_rejects_bad_arguments():
     assert lib.moe_diag_stream_read(aligned, 17, aligned, None) == E_ARG
     assert lib.moe_diag_stream_read(aligned, 16, aligned + 4, None) == E_ARG
     assert lib.moe_diag_stream_read(aligned, 0, aligned, None) == moe.MOE_OK
+
+
+def test_binding_checks_tensors_before_the_abi():
+    """The C-ABI takes plain pointers and cannot see sizes, so the binding
+    rejects a tensor of the wrong dtype, a strided view, a tensor on another
+    device or one with fewer elements than the call uses."""
+    import torch
+    ptr = moe._tensor_ptr
+    bf = moe._bf16_types(torch)
+    cpu = torch.device("cpu")
+    x = torch.zeros(4, 8, dtype=torch.int16)
+    assert ptr(x, "x", 32, bf, cpu) == x.data_ptr()
+    assert ptr(x.view(torch.bfloat16), "x", 32, bf, None) == x.data_ptr()
+    assert ptr(torch.zeros(0, 8, dtype=torch.int16), "x", 0, bf, cpu) is not None
+    bad = [
+        (None, 0, "is None"),
+        (x.view(torch.float16), 32, "dtype"),
+        (x.float(), 32, "dtype"),
+        (x.t(), 32, "contiguous"),
+        (x[:, ::2], 16, "contiguous"),
+        (x, 33, "elements"),
+    ]
+    for t, n, what in bad:
+        with pytest.raises(moe.MoeError, match=what):
+            ptr(t, "x", n, bf, cpu)
+    with pytest.raises(moe.MoeError, match="expected cuda:0"):
+        ptr(x, "x", 32, bf, torch.device("cuda", 0))
+    assert ptr(torch.zeros(16), "wr", 16, (torch.float32,), cpu)
+    with pytest.raises(moe.MoeError, match="dtype"):
+        ptr(torch.zeros(16, dtype=torch.float64), "wr", 16, (torch.float32,), cpu)
+
+
+def test_layer_needs_a_gpu_device():
+    with pytest.raises(moe.MoeError, match="runs on a GPU"):
+        moe.MoeLayer(moe.make_config(256, 128, 8, 2), device="cpu")

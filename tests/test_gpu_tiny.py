@@ -5,6 +5,7 @@ import pytest
 
 import moe_inputs as mi
 import oracle
+import paper_2506_23635_amd as moe
 from harness import (bf16_f64, check_layer_output, host_experts, load_workload_host,
                      make_layer, rel_l2, to_np_u16, x_device)
 
@@ -192,6 +193,38 @@ def _forward(torch, layer, x_t, T=None):
     return to_np_u16(y)
 
 
+def test_binding_rejects_bad_tensors_before_launch(torch_mod, tiny_layer):
+    """A short output, a host tensor, a strided view or a wrong dtype never
+    reaches the library: the call raises and the output stays untouched."""
+    torch = torch_mod
+    wl = TINY.with_(T=8)
+    x_t, _ = x_device(wl)
+    d = wl.d
+    y = torch.full((8, d), 0x3F80, dtype=torch.int16, device="cuda")
+    wide = torch.zeros((8, 2 * d), dtype=torch.int16, device="cuda")
+    cases = [
+        (x_t, y[:7], "elements"),                       # 7 rows for 8 tokens
+        (x_t.cpu(), y, "expected cuda"),
+        (wide[:, ::2], y, "contiguous"),
+        (x_t.view(torch.float16), y, "dtype"),
+        (x_t, y.float(), "dtype"),
+    ]
+    for xa, ya, what in cases:
+        with pytest.raises(moe.MoeError, match=what):
+            tiny_layer.forward(0, xa, ya)
+    with pytest.raises(moe.MoeError, match="elements"):
+        tiny_layer.forward(0, x_t[:4], y, T=8)
+    with pytest.raises(moe.MoeError, match="elements"):
+        tiny_layer.route(0, None, T=8, logits_in=torch.zeros((7, wl.E), device="cuda"))
+    torch.cuda.synchronize()
+    assert bool((y == 0x3F80).all())
+    # bfloat16 tensors are accepted as well as their int16 bits
+    yb = torch.empty((8, d), dtype=torch.bfloat16, device="cuda")
+    tiny_layer.forward(0, x_t.view(torch.bfloat16), yb)
+    torch.cuda.synchronize()
+    assert np.array_equal(to_np_u16(yb.view(torch.int16)), _forward(torch, tiny_layer, x_t))
+
+
 @pytest.mark.parametrize("T", [1, 5, 16])
 def test_forward_decode_path(torch_mod, tiny_layer, T):
     torch = torch_mod
@@ -222,7 +255,6 @@ def test_intermediate_h_within_fp32_error_bound(torch_mod, tiny_layer, T):
     gamma_d * sum|x_i w_i| (gamma_d = d u / (1 - d u), u = 2^-24), carried
     through h = silu(g) u to first order, plus a few fp32 ulps for the
     logistic."""
-    import paper_2506_23635_amd as moe
     torch = torch_mod
     wl = TINY.with_(T=T)
     x_t, x = x_device(wl)
@@ -332,16 +364,21 @@ def test_deterministic_bitwise(torch_mod, tiny_layer):
 
 
 def test_zero_tokens_and_capacity(torch_mod, tiny_layer):
-    import paper_2506_23635_amd as moe
     torch = torch_mod
     x_t = torch.zeros((1, TINY.d), dtype=torch.int16, device="cuda")
     y = torch.full((1, TINY.d), 7, dtype=torch.int16, device="cuda")
     tiny_layer.forward(0, x_t, y, T=0)
     torch.cuda.synchronize()
     assert int(y[0, 0]) == 7           # T == 0 enqueues nothing
+    # buffers that hold 513 tokens pass the binding's checks; the library
+    # rejects T above max_tokens (512) before launching
+    xb = torch.zeros((513, TINY.d), dtype=torch.int16, device="cuda")
+    yb = torch.full((513, TINY.d), 7, dtype=torch.int16, device="cuda")
     with pytest.raises(moe.MoeError) as ei:
-        tiny_layer.forward(0, x_t, y, T=513)
+        tiny_layer.forward(0, xb, yb)
     assert ei.value.status == -4
+    torch.cuda.synchronize()
+    assert bool((yb == 7).all())
 
 
 def test_stack_three_layers(torch_mod):
@@ -370,7 +407,6 @@ def test_diag_stream_read_reads_every_word_once(torch_mod, nbytes):
     equals the XOR of the buffer's 16-byte words (each read once), for sizes
     from one workgroup to a partial last chunk and the unrolled loop's
     remainder."""
-    import paper_2506_23635_amd as moe
     torch = torch_mod
     g = torch.Generator(device="cuda").manual_seed(5)
     buf = torch.randint(-2**31, 2**31 - 1, (nbytes // 4,), dtype=torch.int32, device="cuda", generator=g)
