@@ -340,6 +340,100 @@ def cpu_baseline(wl, budget_s=10.0):
                       f"repetitions, {el:.1f} s of host time, fp64 oracle with OpenMP"}
 
 
+def cpu_oracle_all():
+    """The fp64 oracle on the host cores for every workload, input generation
+    excluded from the clock: the small layer, the decode token, each
+    expert-parallel share at T = 1, 4, 8, and bounded samples of the
+    2048-token prefill layer and of the 32-layer stack (the whole of either
+    takes far longer than a run here: the oracle is deliberately plain).
+    A reported baseline, printed as one JSON line; no GPU is used."""
+    import numpy as np
+    import moe_inputs as mi
+    import oracle
+    model = ""
+    try:
+        with open("/proc/cpuinfo") as fh:
+            model = next((ln.split(":", 1)[1].strip() for ln in fh if ln.startswith("model name")), "")
+    except OSError:
+        pass
+    out = {"metric": "fp64 oracle on the host cores (baseline only)", "cpu_model": model,
+           "nproc": os.cpu_count(), "omp_num_threads": os.environ.get("OMP_NUM_THREADS"),
+           "workloads": {}}
+
+    def experts(wl, ids, layer=0):
+        G, U, D = [None] * wl.E, [None] * wl.E, [None] * wl.E
+        for e in ids:
+            G[e], U[e], D[e] = wl.gate(e, layer), wl.up(e, layer), wl.down(e, layer)
+        return G, U, D
+
+    def clock(fn, min_s=2.0, max_reps=50):
+        reps, t0 = 0, time.perf_counter()
+        while True:
+            fn()
+            reps += 1
+            el = time.perf_counter() - t0
+            if el >= min_s or reps >= max_reps:
+                return el / reps, reps
+
+    def row(name, T, sec, reps, sample, **kw):
+        out["workloads"][name] = {"T": T, "s_per_call": sec, "tokens_per_s": T / sec,
+                                  "reps": reps, "sample": sample, **kw}
+        log(f"oracle {name}: {sec:.3f} s per call")
+
+    wl = mi.WORKLOADS["tiny"]
+    x = wl.x()
+    G, U, D = experts(wl, range(wl.E))
+    sec, reps = clock(lambda: oracle.layer(x, wl.router(), wl.bias(), G, U, D, wl.k))
+    row("tiny", wl.T, sec, reps, "the whole layer (16 tokens)")
+
+    wl = mi.WORKLOADS["decode"]
+    x, wr = wl.x(), wl.router()
+    idx, _ = oracle.route_from_logits(oracle.router_logits(x, wr), wl.k)
+    G, U, D = experts(wl, sorted(set(idx.reshape(-1).tolist())))
+    sec, reps = clock(lambda: oracle.layer(x, wr, wl.bias(), G, U, D, wl.k), min_s=5.0)
+    row("decode", 1, sec, reps, "the whole layer (1 token, 4 experts)")
+
+    sw = mi.WORKLOADS["ep_share"]
+    wr = sw.router()
+    for s in range(4):
+        G, U, D = experts(sw, range(4 * s, 4 * s + 4))
+        for T in (1, 4, 8):
+            x = mi.gen_bf16(sw.seed, mi.stream_id(mi.KIND_X), (T, sw.d), sw.sigma_x)
+            idx, _ = oracle.route_from_logits(oracle.router_logits(x, wr), sw.k)
+            touched = len({e for e in idx.reshape(-1).tolist() if 4 * s <= e < 4 * s + 4})
+            sec, reps = clock(lambda: oracle.layer(x, wr, None, G, U, D, sw.k, e_begin=4 * s,
+                                                   n_local=4), min_s=1.0, max_reps=10)
+            row(f"ep_share{s}_T{T}", T, sec, reps, "the whole share (layer 0)",
+                local_experts_touched=touched)
+
+    wl = mi.WORKLOADS["prefill"]
+    n = 8
+    x = wl.x()[:n]
+    idx, _ = oracle.route_from_logits(oracle.router_logits(x, wl.router(), wl.bias()), wl.k)
+    G, U, D = experts(wl, sorted(set(idx.reshape(-1).tolist())))
+    sec, reps = clock(lambda: oracle.layer(x, wl.router(), wl.bias(), G, U, D, wl.k), min_s=0.0,
+                      max_reps=1)
+    row("prefill", n, sec, reps, f"the first {n} of the 2048 tokens through the whole layer; "
+        f"the full layer scales with the tokens (x {wl.T // n})")
+    del G, U, D
+
+    wl = mi.WORKLOADS["stack"]
+    n_l = 2
+    x = wl.x()
+    sec = 0.0
+    for li in range(n_l):
+        wr = wl.router(li)
+        idx, _ = oracle.route_from_logits(oracle.router_logits(x, wr), wl.k)
+        G, U, D = experts(wl, sorted(set(idx.reshape(-1).tolist())), li)
+        t0 = time.perf_counter()
+        r = oracle.layer(x, wr, None, G, U, D, wl.k)
+        x = oracle.residual_add(x, r["y"])
+        sec += time.perf_counter() - t0
+    row("stack", wl.T, sec * wl.n_layers / n_l, 1,
+        f"the first {n_l} of the 32 layers, scaled to the step (x {wl.n_layers // n_l})")
+    print(json.dumps(out), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -355,7 +449,12 @@ def main():
                     help="time only the prefill layer (for counter collection)")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="also run one 1 GiB device copy of known size (counter calibration)")
+    ap.add_argument("--cpu-oracle-all", action="store_true",
+                    help="only time the fp64 oracle on every workload on the host (no GPU)")
     args = ap.parse_args()
+    if args.cpu_oracle_all:
+        cpu_oracle_all()
+        return
     if args.gpus != 1:
         print(f"bench.py measures one GPU only: this build has no multi-GPU path "
               f"(--gpus {args.gpus} requested)", file=sys.stderr)
