@@ -407,7 +407,7 @@ def cpu_oracle_all():
                 local_experts_touched=touched)
 
     wl = mi.WORKLOADS["prefill"]
-    n = 8
+    n = 64
     x = wl.x()[:n]
     idx, _ = oracle.route_from_logits(oracle.router_logits(x, wl.router(), wl.bias()), wl.k)
     G, U, D = experts(wl, sorted(set(idx.reshape(-1).tolist())))
@@ -418,7 +418,7 @@ def cpu_oracle_all():
     del G, U, D
 
     wl = mi.WORKLOADS["stack"]
-    n_l = 2
+    n_l = 8
     x = wl.x()
     sec = 0.0
     for li in range(n_l):
