@@ -217,7 +217,7 @@ MOE_API const char *moe_status_string(moe_status s);
  * Enqueued on stream; allocates nothing.  src and out 16-byte aligned and
  * bytes a multiple of 16, else MOE_E_ARG (nothing enqueued); bytes == 0
  * enqueues nothing. */
-#define MOE_DIAG_MAX_WG 2048
+#define MOE_DIAG_MAX_WG 512
 MOE_API moe_status moe_diag_stream_read(const void *src, uint64_t bytes, uint32_t *out,
                                         moe_stream_t stream);
 

@@ -16,7 +16,7 @@ PKG_DIR = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(PKG_DIR, "libmoe.so")
 
 MOE_OK = 0
-DIAG_MAX_WG = 2048   # MOE_DIAG_MAX_WG of include/moe.h
+DIAG_MAX_WG = 512    # MOE_DIAG_MAX_WG of include/moe.h
 STATUS_NAMES = {0: "MOE_OK", -1: "MOE_E_ARG", -2: "MOE_E_SHAPE", -3: "MOE_E_ALIGN",
                 -4: "MOE_E_CAPACITY", -5: "MOE_E_STATE", -6: "MOE_E_HIP"}
 

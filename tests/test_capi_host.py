@@ -181,3 +181,10 @@ def test_binding_checks_tensors_before_the_abi():
 def test_layer_needs_a_gpu_device():
     with pytest.raises(moe.MoeError, match="runs on a GPU"):
         moe.MoeLayer(moe.make_config(256, 128, 8, 2), device="cpu")
+
+
+def test_binding_constants_match_the_header():
+    text = open(HEADER).read()
+    assert int(re.search(r"#define MOE_DIAG_MAX_WG (\d+)", text).group(1)) == moe.DIAG_MAX_WG
+    for name, value in moe.STATUS_NAMES.items():
+        assert re.search(rf"\b{value}\s*=\s*{name}\b", text), value
