@@ -1,10 +1,11 @@
 // moe_decode.hip -- the expert FFN for small token counts (decode: at most 16
 // tokens per expert), streamed from HBM.
 //
-// Each workgroup owns one 16-feature tile of one active expert; its kSplit
-// waves each walk a contiguous 1/kSplit of the reduction dimension, and wave
-// 0 adds the partial fragments in wave order (deterministic) before the
-// epilogue.  Splitting K keeps enough loads in flight when few experts are
+// Each workgroup owns one 16-feature tile of one active expert; wave w of its
+// kSplit waves takes the K tiles w, w + kSplit, w + 2 kSplit, ... (so at each
+// step the waves together read kSplit * kUnroll consecutive 1 KiB tiles of
+// the slab), and wave 0 adds the partial fragments in wave order
+// (deterministic) before the epilogue.  Splitting K keeps enough loads in flight when few experts are
 // active (one expert of an expert-parallel share has only 672 gate/up and 384
 // down tiles).  The weight tile is the A operand of v_mfma_f32_16x16x32_bf16
 // and the (at most 16) tokens of the expert are the B operand, so the matrix
@@ -24,13 +25,6 @@ namespace moe {
 
 constexpr int kSplit = 8;    // waves per workgroup (K split)
 constexpr int kUnroll = 8;
-
-// K tiles [kt0, kt1) of wave w: contiguous, sizes differ by at most one
-__device__ inline void k_range(int KT, int w, int& kt0, int& kt1)
-{
-    kt0 = KT * w / kSplit;
-    kt1 = KT * (w + 1) / kSplit;
-}
 
 // partial fragments of waves 1.. through LDS; wave 0 adds them in wave order
 __device__ inline void reduce_waves(f32x4_t& v, f32x4_t* s, int w, int lane)
@@ -76,25 +70,26 @@ __global__ __launch_bounds__(64 * kSplit) void gateup_kernel(DecodeArgs a)
     f32x4_t acc_g = {0.f, 0.f, 0.f, 0.f};
     f32x4_t acc_u = {0.f, 0.f, 0.f, 0.f};
     const u32x4_t zero = {0u, 0u, 0u, 0u};
-    int kt, kt1;
-    k_range(KT, w, kt, kt1);
-    for (; kt + kUnroll <= kt1; kt += kUnroll) {
+    // wave w takes K tiles w, w + kSplit, ...: per step the workgroup's waves
+    // read kSplit * kUnroll consecutive tiles of each slab
+    int kt = 0;
+    for (; kt + kSplit * kUnroll <= KT; kt += kSplit * kUnroll) {
         u32x4_t wg[kUnroll], wu[kUnroll], xb[kUnroll];
 #pragma unroll
         for (int u = 0; u < kUnroll; ++u) {
-            wg[u] = ld16(pg + (int64_t)(kt + u) * kTileBytes);
-            wu[u] = ld16(pu + (int64_t)(kt + u) * kTileBytes);
+            wg[u] = ld16(pg + (int64_t)(kt + w + kSplit * u) * kTileBytes);
+            wu[u] = ld16(pu + (int64_t)(kt + w + kSplit * u) * kTileBytes);
         }
 #pragma unroll
         for (int u = 0; u < kUnroll; ++u)
-            xb[u] = has_tok ? ld16_cached(px + (kt + u) * kTileK) : zero;
+            xb[u] = has_tok ? ld16_cached(px + (kt + w + kSplit * u) * kTileK) : zero;
 #pragma unroll
         for (int u = 0; u < kUnroll; ++u) {
             acc_g = mfma16x16x32(wg[u], xb[u], acc_g);
             acc_u = mfma16x16x32(wu[u], xb[u], acc_u);
         }
     }
-    for (; kt < kt1; ++kt) {
+    for (kt += w; kt < KT; kt += kSplit) {
         const u32x4_t wg = ld16(pg + (int64_t)kt * kTileBytes), wu = ld16(pu + (int64_t)kt * kTileBytes);
         const u32x4_t xb = has_tok ? ld16_cached(px + kt * kTileK) : zero;
         acc_g = mfma16x16x32(wg, xb, acc_g);
@@ -136,19 +131,19 @@ __global__ __launch_bounds__(64 * kSplit) void down_kernel(DecodeArgs a)
 
     f32x4_t acc = {0.f, 0.f, 0.f, 0.f};
     const u32x4_t zero = {0u, 0u, 0u, 0u};
-    int kt, kt1;
-    k_range(KT, w, kt, kt1);
-    for (; kt + kUnroll <= kt1; kt += kUnroll) {
+    int kt = 0;
+    for (; kt + kSplit * kUnroll <= KT; kt += kSplit * kUnroll) {
         u32x4_t wv[kUnroll], hb[kUnroll];
 #pragma unroll
-        for (int u = 0; u < kUnroll; ++u) wv[u] = ld16(pw + (int64_t)(kt + u) * kTileBytes);
+        for (int u = 0; u < kUnroll; ++u)
+            wv[u] = ld16(pw + (int64_t)(kt + w + kSplit * u) * kTileBytes);
 #pragma unroll
         for (int u = 0; u < kUnroll; ++u)
-            hb[u] = has_tok ? ld16_cached(ph + (kt + u) * kTileK) : zero;
+            hb[u] = has_tok ? ld16_cached(ph + (kt + w + kSplit * u) * kTileK) : zero;
 #pragma unroll
         for (int u = 0; u < kUnroll; ++u) acc = mfma16x16x32(wv[u], hb[u], acc);
     }
-    for (; kt < kt1; ++kt) {
+    for (kt += w; kt < KT; kt += kSplit) {
         const u32x4_t wv = ld16(pw + (int64_t)kt * kTileBytes);
         const u32x4_t hb = has_tok ? ld16_cached(ph + kt * kTileK) : zero;
         acc = mfma16x16x32(wv, hb, acc);
