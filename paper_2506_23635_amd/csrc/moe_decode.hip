@@ -3,11 +3,11 @@
 //
 // Each workgroup owns one 16-feature tile of one active expert; wave w of its
 // kSplit waves takes the K tiles w, w + kSplit, w + 2 kSplit, ... (so at each
-// step the waves together read kSplit * kUnroll consecutive 1 KiB tiles of
+// step the waves together read kSplit x unroll consecutive 1 KiB tiles of
 // the slab), and wave 0 adds the partial fragments in wave order
-// (deterministic) before the epilogue.  Splitting K keeps enough loads in flight when few experts are
-// active (one expert of an expert-parallel share has only 672 gate/up and 384
-// down tiles).  The weight tile is the A operand of v_mfma_f32_16x16x32_bf16
+// (deterministic) before the epilogue.  Splitting K keeps enough loads in
+// flight when few experts are active (one expert of an expert-parallel share
+// has only 672 gate/up and 384 down tiles).  The weight tile is the A operand of v_mfma_f32_16x16x32_bf16
 // and the (at most 16) tokens of the expert are the B operand, so the matrix
 // cores do the dot products and the reduction over K; the kernel is a pure
 // 16-byte-per-lane stream of the packed weights (every wave-wide load is 1 KiB
@@ -24,7 +24,11 @@
 namespace moe {
 
 constexpr int kSplit = 8;    // waves per workgroup (K split)
-constexpr int kUnroll = 8;
+// K tiles per wave per step (loads in flight per slab and wave).  Measured
+// on the decode step: gate/up is flat over 4..8; down is fastest at 6 (8 and
+// 12 hold more registers for no gain, 2..4 keep too few loads in flight).
+constexpr int kUnrollGU = 8;
+constexpr int kUnrollDN = 6;
 
 // partial fragments of waves 1.. through LDS; wave 0 adds them in wave order
 __device__ inline void reduce_waves(f32x4_t& v, f32x4_t* s, int w, int lane)
@@ -71,20 +75,20 @@ __global__ __launch_bounds__(64 * kSplit) void gateup_kernel(DecodeArgs a)
     f32x4_t acc_u = {0.f, 0.f, 0.f, 0.f};
     const u32x4_t zero = {0u, 0u, 0u, 0u};
     // wave w takes K tiles w, w + kSplit, ...: per step the workgroup's waves
-    // read kSplit * kUnroll consecutive tiles of each slab
+    // read kSplit * kUnrollGU consecutive tiles of each slab
     int kt = 0;
-    for (; kt + kSplit * kUnroll <= KT; kt += kSplit * kUnroll) {
-        u32x4_t wg[kUnroll], wu[kUnroll], xb[kUnroll];
+    for (; kt + kSplit * kUnrollGU <= KT; kt += kSplit * kUnrollGU) {
+        u32x4_t wg[kUnrollGU], wu[kUnrollGU], xb[kUnrollGU];
 #pragma unroll
-        for (int u = 0; u < kUnroll; ++u) {
+        for (int u = 0; u < kUnrollGU; ++u) {
             wg[u] = ld16(pg + (int64_t)(kt + w + kSplit * u) * kTileBytes);
             wu[u] = ld16(pu + (int64_t)(kt + w + kSplit * u) * kTileBytes);
         }
 #pragma unroll
-        for (int u = 0; u < kUnroll; ++u)
+        for (int u = 0; u < kUnrollGU; ++u)
             xb[u] = has_tok ? ld16_cached(px + (kt + w + kSplit * u) * kTileK) : zero;
 #pragma unroll
-        for (int u = 0; u < kUnroll; ++u) {
+        for (int u = 0; u < kUnrollGU; ++u) {
             acc_g = mfma16x16x32(wg[u], xb[u], acc_g);
             acc_u = mfma16x16x32(wu[u], xb[u], acc_u);
         }
@@ -132,16 +136,16 @@ __global__ __launch_bounds__(64 * kSplit) void down_kernel(DecodeArgs a)
     f32x4_t acc = {0.f, 0.f, 0.f, 0.f};
     const u32x4_t zero = {0u, 0u, 0u, 0u};
     int kt = 0;
-    for (; kt + kSplit * kUnroll <= KT; kt += kSplit * kUnroll) {
-        u32x4_t wv[kUnroll], hb[kUnroll];
+    for (; kt + kSplit * kUnrollDN <= KT; kt += kSplit * kUnrollDN) {
+        u32x4_t wv[kUnrollDN], hb[kUnrollDN];
 #pragma unroll
-        for (int u = 0; u < kUnroll; ++u)
+        for (int u = 0; u < kUnrollDN; ++u)
             wv[u] = ld16(pw + (int64_t)(kt + w + kSplit * u) * kTileBytes);
 #pragma unroll
-        for (int u = 0; u < kUnroll; ++u)
+        for (int u = 0; u < kUnrollDN; ++u)
             hb[u] = has_tok ? ld16_cached(ph + (kt + w + kSplit * u) * kTileK) : zero;
 #pragma unroll
-        for (int u = 0; u < kUnroll; ++u) acc = mfma16x16x32(wv[u], hb[u], acc);
+        for (int u = 0; u < kUnrollDN; ++u) acc = mfma16x16x32(wv[u], hb[u], acc);
     }
     for (kt += w; kt < KT; kt += kSplit) {
         const u32x4_t wv = ld16(pw + (int64_t)kt * kTileBytes);
