@@ -30,12 +30,71 @@ def log(msg):
     print(msg, file=sys.stderr, flush=True)
 
 
+# One device allocation made before any section runs; every section carves
+# its weight arena, workspace and staging buffers from it after a reset.
+# Measured: an arena allocated into memory that an earlier section had
+# allocated and freed streams 2-4 % slower (the decode step after the 4 GiB
+# read buffer 249.3 vs 239.5 us, expert-parallel shares after the decode
+# layer up to 4 %), so without the pool each figure would depend on what ran
+# before it in the process.
+_POOL = None
+_POOL_OFF = 0
+
+
+def pool_init(nbytes):
+    global _POOL, _POOL_OFF
+    import torch
+    _POOL = torch.empty(nbytes, dtype=torch.uint8, device="cuda")
+    _POOL_OFF = 0
+
+
+def pool_reset():
+    """Starts a section: the previous section's work has finished before
+    its memory is handed out again."""
+    global _POOL_OFF
+    import torch
+    torch.cuda.synchronize()
+    _POOL_OFF = 0
+
+
+def pool_take(nbytes):
+    """A 256-byte-aligned uint8 view of the pool (a plain allocation when
+    no pool was made, e.g. for helper scripts)."""
+    global _POOL_OFF
+    import torch
+    if _POOL is None:
+        return torch.empty(nbytes, dtype=torch.uint8, device="cuda")
+    off = (_POOL_OFF + 255) // 256 * 256
+    if off + nbytes > _POOL.numel():
+        raise RuntimeError(f"bench pool exhausted ({off + nbytes} of {_POOL.numel()} bytes)")
+    _POOL_OFF = off + nbytes
+    return _POOL[off: off + nbytes]
+
+
+def pool_layer(cfg):
+    import paper_2506_23635_amd as moe
+    return moe.MoeLayer(cfg, arena=pool_take(moe.moe_weight_bytes(cfg)),
+                        workspace=pool_take(moe.moe_workspace_bytes(cfg)))
+
+
+def staging_buffer(wl):
+    import torch
+    return pool_take(3 * wl.d * wl.f * 2).view(torch.int16)
+
+
+def section_bytes(cfg, wl):
+    """Pool bytes one section takes: arena, workspace, staging, alignment."""
+    import paper_2506_23635_amd as moe
+    return moe.moe_weight_bytes(cfg) + moe.moe_workspace_bytes(cfg) + 3 * wl.d * wl.f * 2 + 1024
+
+
 def setup_layer(wl, max_tokens):
     import torch
     import moe_inputs as mi
     import paper_2506_23635_amd as moe
     cfg = moe.make_config(wl.d, wl.f, wl.E, wl.k, max_tokens=max_tokens)
-    layer = moe.MoeLayer(cfg)
+    pool_reset()
+    layer = pool_layer(cfg)
     s = layer.stream
     d, f, E = wl.d, wl.f, wl.E
     wr = torch.empty(d * E, dtype=torch.float32, device="cuda")
@@ -45,7 +104,7 @@ def setup_layer(wl, max_tokens):
         b = torch.empty(E, dtype=torch.float32, device="cuda")
         mi.gen_f32_device(wl.seed, mi.stream_id(mi.KIND_BIAS), E, wl.sigma_b, b.data_ptr(), s)
     layer.load_router(0, wr, b)
-    stg = torch.empty(3 * d * f, dtype=torch.int16, device="cuda")
+    stg = staging_buffer(wl)
     g, u, dn = stg[: d * f], stg[d * f: 2 * d * f], stg[2 * d * f:]
     for e in range(E):
         mi.gen_bf16_device(wl.seed, mi.stream_id(mi.KIND_GATE, 0, e), d * f, wl.sigma_w, g.data_ptr(), s)
@@ -156,12 +215,13 @@ def ep_share_section(steps):
     sw = mi.WORKLOADS["ep_share"]
     n_rot = 4
     expert_bytes = 3 * sw.d * sw.f * 2
-    staging = torch.empty(3 * sw.d * sw.f, dtype=torch.int16, device="cuda")
     rows = []
     for s in range(4):
         cfg = moe.make_config(sw.d, sw.f, sw.E, sw.k, expert_begin=4 * s, n_local_experts=4,
                               n_layers=n_rot, max_tokens=8)
-        layer = moe.MoeLayer(cfg)
+        pool_reset()
+        layer = pool_layer(cfg)
+        staging = staging_buffer(sw)
         for li in range(n_rot):
             load_layer_device(layer, sw, li, li, staging)
         torch.cuda.synchronize()
@@ -198,8 +258,7 @@ def ep_share_section(steps):
                          "hbm_gbs": (bytes_step / (ms * 1e-3) / 1e9) if sum(touched) else None})
             log(f"ep share {s} T={T}: {ms * 1e3:.1f} us graph, {ms_direct * 1e3:.1f} direct, touched {touched}")
         layer.close()
-        del layer
-    del staging
+        del layer, staging
     torch.cuda.empty_cache()
     return rows
 
@@ -211,15 +270,16 @@ def stack_section(steps, warmup):
     import moe_inputs as mi
     import paper_2506_23635_amd as moe
     sw = mi.WORKLOADS["stack"]
-    free, _ = torch.cuda.mem_get_info()
     expert_bytes = 3 * sw.d * sw.f * 2
-    need = sw.n_layers * sw.E * expert_bytes + (8 << 30)
-    if free < need:
-        log(f"stack: skipped ({free / 1e9:.0f} GB free, {need / 1e9:.0f} GB needed)")
-        return None
     cfg = moe.make_config(sw.d, sw.f, sw.E, sw.k, n_layers=sw.n_layers, max_tokens=sw.T)
-    layer = moe.MoeLayer(cfg)
-    staging = torch.empty(3 * sw.d * sw.f, dtype=torch.int16, device="cuda")
+    need = section_bytes(cfg, sw)
+    have = _POOL.numel() if _POOL is not None else torch.cuda.mem_get_info()[0] - (8 << 30)
+    if have < need:
+        log(f"stack: skipped ({have / 1e9:.0f} GB available, {need / 1e9:.0f} GB needed)")
+        return None
+    pool_reset()
+    layer = pool_layer(cfg)
+    staging = staging_buffer(sw)
     t0 = time.perf_counter()
     for li in range(sw.n_layers):
         load_layer_device(layer, sw, li, li, staging)
@@ -275,7 +335,8 @@ def stream_read_gbs(nbytes=4 << 30, reps=20):
     read rate, reported beside the 8 TB/s spec peak."""
     import torch
     import paper_2506_23635_amd as moe
-    buf = torch.empty(nbytes, dtype=torch.uint8, device="cuda")
+    pool_reset()
+    buf = pool_take(nbytes)
     out = torch.zeros(4 * moe.DIAG_MAX_WG, dtype=torch.int32, device="cuda")
     s = torch.cuda.current_stream().cuda_stream
     for _ in range(3):
@@ -468,14 +529,27 @@ def main():
     import paper_2506_23635_amd as moe
     moe.lib()   # raises if the HIP library is not built
 
+    # the device pool, sized for the largest section that will run
+    def cfg_of(w, **kw):
+        return moe.make_config(w.d, w.f, w.E, w.k, **kw)
+    dw, pw0, sw0, kw0 = (mi.WORKLOADS[n] for n in ("decode", "prefill", "ep_share", "stack"))
+    sizes = [4 << 30, 2 << 30, section_bytes(cfg_of(dw, max_tokens=dw.T), dw)]
+    if not args.no_prefill or args.prefill_only:
+        sizes.append(section_bytes(cfg_of(pw0, max_tokens=pw0.T), pw0))
+    if not args.no_ep_share:
+        sizes.append(section_bytes(cfg_of(sw0, expert_begin=0, n_local_experts=4, n_layers=4,
+                                          max_tokens=8), sw0))
+    if not args.no_stack and not args.prefill_only:
+        stack_need = section_bytes(cfg_of(kw0, n_layers=kw0.n_layers, max_tokens=kw0.T), kw0)
+        if stack_need + (8 << 30) <= torch.cuda.mem_get_info()[0]:
+            sizes.append(stack_need)
+    pool_init(max(sizes))
+
     if args.calibrate_copy:
-        src = torch.empty(1 << 30, dtype=torch.uint8, device="cuda")
-        dst = torch.empty_like(src)
-        torch.cuda.synchronize()
+        pool_reset()
+        src, dst = pool_take(1 << 30), pool_take(1 << 30)
         dst.copy_(src)          # reads 1 GiB, writes 1 GiB
-        torch.cuda.synchronize()
-        del src, dst
-        torch.cuda.empty_cache()
+        pool_reset()
     if args.prefill_only:
         pw = mi.WORKLOADS["prefill"]
         player, px = setup_layer(pw, max_tokens=pw.T)
@@ -486,10 +560,6 @@ def main():
               flush=True)
         player.close()
         return
-
-    log("timing the plain streaming read (4 GiB) ...")
-    read_gbs = stream_read_gbs()
-    log(f"streaming read {read_gbs:.0f} GB/s")
 
     wl = mi.WORKLOADS["decode"]
     log("setup decode layer (16 experts, 6.3 GB) ...")
@@ -512,7 +582,9 @@ def main():
     gu_gbs = gu_bytes / (gu["ms_per_launch"] * 1e-3) / 1e9
     layer.close()
     del layer, x
-    torch.cuda.empty_cache()
+    log("timing the plain streaming read (4 GiB) ...")
+    read_gbs = stream_read_gbs()
+    log(f"streaming read {read_gbs:.0f} GB/s")
 
     prefill = None
     if not args.no_prefill:
