@@ -85,7 +85,7 @@ def staging_buffer(wl):
 def section_bytes(cfg, wl):
     """Pool bytes one section takes: arena, workspace, staging, alignment."""
     import paper_2506_23635_amd as moe
-    return moe.moe_weight_bytes(cfg) + moe.moe_workspace_bytes(cfg) + 3 * wl.d * wl.f * 2 + 1024
+    return moe.moe_weight_bytes(cfg) + moe.moe_workspace_bytes(cfg) + 3 * wl.d * wl.f * 2 + (16 << 20)
 
 
 def setup_layer(wl, max_tokens):
