@@ -120,7 +120,10 @@ MOE_API size_t moe_workspace_bytes(const moe_config *cfg);
 
 /* Validates cfg, records the caller-allocated device buffers (sizes from the
  * functions above; they must stay allocated and unmoved until moe_destroy)
- * and returns a new context in *out.  Allocates only the host-side context. */
+ * and returns a new context in *out.  Allocates only the host-side context.
+ * The weight stream is sensitive to where the arena lands: measured, an arena
+ * placed in memory that earlier allocations had used and freed streams 2-4 %
+ * slower than one carved from a single large allocation made up front. */
 MOE_API moe_status moe_init(const moe_config *cfg, void *weight_arena, void *workspace,
                     moe_ctx **out);
 
