@@ -252,10 +252,22 @@ def ep_share_section(steps):
             # one replay runs the 4 rotating layers
             ms = graph_ms(step, max(n // n_rot, 5), 2) / n_rot
             bytes_step = sum(touched) / n_rot * expert_bytes + sw.d * sw.E * 4
+            # the rate over the layers that touch a local expert: a layer with
+            # none (routing and combine only, no weights) is timed alone, as
+            # its own graph, and its time taken out
+            idle_ms = 0.0
+            for li in range(n_rot):
+                if touched[li] == 0:
+                    idle_ms += graph_ms(lambda li=li: layer.forward(li, x, y), 40, 5)
+            busy = [li for li in range(n_rot) if touched[li] > 0]
+            busy_ms = ms * n_rot - idle_ms
             rows.append({"share": s, "experts": [4 * s, 4 * s + 3], "T": T,
                          "local_experts_touched": touched, "us_per_step": ms * 1e3,
                          "us_per_step_direct_launch": ms_direct * 1e3,
-                         "hbm_gbs": (bytes_step / (ms * 1e-3) / 1e9) if sum(touched) else None})
+                         "hbm_gbs": (bytes_step / (ms * 1e-3) / 1e9) if sum(touched) else None,
+                         "hbm_gbs_touched_layers":
+                             ((sum(touched) * expert_bytes + len(busy) * sw.d * sw.E * 4)
+                              / (busy_ms * 1e-3) / 1e9) if busy else None})
             log(f"ep share {s} T={T}: {ms * 1e3:.1f} us graph, {ms_direct * 1e3:.1f} direct, touched {touched}")
         layer.close()
         del layer, staging
