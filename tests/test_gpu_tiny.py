@@ -225,6 +225,31 @@ def test_binding_rejects_bad_tensors_before_launch(torch_mod, tiny_layer):
     assert np.array_equal(to_np_u16(yb.view(torch.int16)), _forward(torch, tiny_layer, x_t))
 
 
+def test_binding_rejects_bad_weights_before_load(torch_mod, tiny_layer):
+    """Weight loads are checked like activations: a short matrix, weights
+    split between host and device, a wrong router dtype or a short bias
+    raise before anything is copied, and the loaded layer is unchanged."""
+    torch = torch_mod
+    wl = TINY
+    d, f, E = wl.d, wl.f, wl.E
+    x_t, _ = x_device(wl)
+    before = _forward(torch, tiny_layer, x_t)
+    g = torch.zeros(d * f, dtype=torch.int16, device="cuda")
+    cases = [
+        (lambda: tiny_layer.load_expert(0, 0, g[:-1], g, g), "elements"),
+        (lambda: tiny_layer.load_expert(0, 0, g, g.cpu(), g), "all on the GPU or all on the host"),
+        (lambda: tiny_layer.load_expert(0, 0, g.view(torch.float16), g, g), "dtype"),
+        (lambda: tiny_layer.load_router(0, torch.zeros(d * E, dtype=torch.float64, device="cuda")),
+         "dtype"),
+        (lambda: tiny_layer.load_router(0, torch.zeros(d * E, device="cuda"),
+                                        torch.zeros(E - 1, device="cuda")), "elements"),
+    ]
+    for call, what in cases:
+        with pytest.raises(moe.MoeError, match=what):
+            call()
+    assert np.array_equal(_forward(torch, tiny_layer, x_t), before)
+
+
 @pytest.mark.parametrize("T", [1, 5, 16])
 def test_forward_decode_path(torch_mod, tiny_layer, T):
     torch = torch_mod
