@@ -22,6 +22,7 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 METRIC = "DBRX-shape MoE layer: decode µs/layer + HBM GB/s; prefill tokens/s + MFMA %"
+N_ROT = 4                      # independently seeded layers the decode timing rotates over
 HBM_PEAK_GBS = 8000.0          # MI355X HBM3E, GB/s
 MFMA_BF16_PEAK_TFLOPS = 2500.0  # MI355X dense bf16 matrix, TFLOP/s
 
@@ -71,6 +72,19 @@ def pool_take(nbytes):
     return _POOL[off: off + nbytes]
 
 
+def pool_release():
+    """Ends the run's device work explicitly: waits for the stream, drops the
+    pool and returns torch's cached blocks, so that no device memory is freed
+    during interpreter shutdown (after a profiler's own exit handlers)."""
+    global _POOL, _POOL_OFF
+    import torch
+    torch.cuda.synchronize()
+    _POOL = None
+    _POOL_OFF = 0
+    torch.cuda.empty_cache()
+    torch.cuda.synchronize()
+
+
 def pool_layer(cfg):
     import paper_2506_23635_amd as moe
     return moe.MoeLayer(cfg, arena=pool_take(moe.moe_weight_bytes(cfg)),
@@ -118,20 +132,45 @@ def setup_layer(wl, max_tokens):
     return layer, x.view(wl.T, d)
 
 
-def time_layer(layer, x, steps, warmup, kernel_events=True):
-    """Runs warmup + timed steps; returns (ms_per_step, per-kernel ms/launch, counts)."""
+def setup_rotation(wl, n_rot, max_tokens):
+    """The whole 16-expert layer held n_rot times, each copy an independently
+    seeded layer (router and experts of layer index 0..n_rot-1), so that a
+    timed step rotating over them re-reads no weight byte within
+    (n_rot - 1) layers (~19 GB at DBRX shape): the 256 MB last-level cache
+    cannot serve repeats.  The input x is the same for every copy."""
+    import torch
+    import moe_inputs as mi
+    import paper_2506_23635_amd as moe
+    cfg = moe.make_config(wl.d, wl.f, wl.E, wl.k, n_layers=n_rot, max_tokens=max_tokens)
+    pool_reset()
+    layer = pool_layer(cfg)
+    staging = staging_buffer(wl)
+    for li in range(n_rot):
+        load_layer_device(layer, wl, li, li, staging)
+    x = torch.empty(wl.T * wl.d, dtype=torch.int16, device="cuda")
+    mi.gen_bf16_device(wl.seed, mi.stream_id(mi.KIND_X), wl.T * wl.d, wl.sigma_x, x.data_ptr(),
+                       layer.stream)
+    torch.cuda.synchronize()
+    del staging
+    return layer, x.view(wl.T, wl.d)
+
+
+def time_layer(layer, x, steps, warmup, kernel_events=True, n_rot=1):
+    """Runs warmup + timed steps, step i on arena layer i % n_rot; returns
+    (ms_per_step, per-kernel ms/launch, routing of layer 0, dropped)."""
     import torch
     import paper_2506_23635_amd as moe
     T = x.shape[0]
     y = torch.empty((T, layer.cfg.d_model), dtype=torch.int16, device="cuda")
-    for _ in range(warmup):
-        layer.forward(0, x, y)
+    for i in range(max(warmup, n_rot)):
+        layer.forward(i % n_rot, x, y)
     torch.cuda.synchronize()
+    steps = max(steps - steps % n_rot, n_rot)
     moe.moe_profile_enable(layer.ctx, 8 * steps + 8 if kernel_events else 0)
     torch.cuda.synchronize()
     t0 = time.perf_counter()
-    for _ in range(steps):
-        layer.forward(0, x, y)
+    for i in range(steps):
+        layer.forward(i % n_rot, x, y)
     torch.cuda.synchronize()
     t1 = time.perf_counter()
     prof, dropped = moe.moe_profile_read(layer.ctx)
@@ -178,7 +217,12 @@ def load_layer_device(layer, wl, layer_idx, arena_layer, staging):
     wr = torch.empty(d * E, dtype=torch.float32, device="cuda")
     mi.gen_f32_device(wl.seed, mi.stream_id(mi.KIND_ROUTER, layer_idx), d * E, wl.sigma_r,
                       wr.data_ptr(), s)
-    layer.load_router(arena_layer, wr, None)
+    b = None
+    if wl.sigma_b:
+        b = torch.empty(E, dtype=torch.float32, device="cuda")
+        mi.gen_f32_device(wl.seed, mi.stream_id(mi.KIND_BIAS, layer_idx), E, wl.sigma_b,
+                          b.data_ptr(), s)
+    layer.load_router(arena_layer, wr, b)
     g, u, dn = staging[: d * f], staging[d * f: 2 * d * f], staging[2 * d * f:]
     c = layer.cfg
     for e in range(c.expert_begin, c.expert_begin + c.n_local_experts):
@@ -406,11 +450,22 @@ def cpu_baseline(wl, budget_s=10.0):
         el = time.perf_counter() - t0
         if el >= budget_s or reps >= 1000:
             break
-    threads = int(os.environ.get("OMP_NUM_THREADS", "0") or 0) or os.cpu_count()
+    omp = os.environ.get("OMP_NUM_THREADS")
+    threads = int(omp or 0) or os.cpu_count()
     assert np.isfinite(el)
     return {"value": reps * wl.T / el, "unit": "tokens/s", "cores": threads, "kind": "oracle",
+            "cpu_model": cpu_model(), "omp_num_threads": omp, "nproc": os.cpu_count(),
             "sample": f"decode token (T={wl.T}) through the full 16-expert layer, {reps} "
                       f"repetitions, {el:.1f} s of host time, fp64 oracle with OpenMP"}
+
+
+def cpu_model():
+    try:
+        with open("/proc/cpuinfo") as fh:
+            return next((ln.split(":", 1)[1].strip() for ln in fh if ln.startswith("model name")),
+                        "")
+    except OSError:
+        return ""
 
 
 def cpu_oracle_all():
@@ -423,13 +478,7 @@ def cpu_oracle_all():
     import numpy as np
     import moe_inputs as mi
     import oracle
-    model = ""
-    try:
-        with open("/proc/cpuinfo") as fh:
-            model = next((ln.split(":", 1)[1].strip() for ln in fh if ln.startswith("model name")), "")
-    except OSError:
-        pass
-    out = {"metric": "fp64 oracle on the host cores (baseline only)", "cpu_model": model,
+    out = {"metric": "fp64 oracle on the host cores (baseline only)", "cpu_model": cpu_model(),
            "nproc": os.cpu_count(), "omp_num_threads": os.environ.get("OMP_NUM_THREADS"),
            "workloads": {}}
 
@@ -545,7 +594,8 @@ def main():
     def cfg_of(w, **kw):
         return moe.make_config(w.d, w.f, w.E, w.k, **kw)
     dw, pw0, sw0, kw0 = (mi.WORKLOADS[n] for n in ("decode", "prefill", "ep_share", "stack"))
-    sizes = [4 << 30, 2 << 30, section_bytes(cfg_of(dw, max_tokens=dw.T), dw)]
+    sizes = [4 << 30, 2 << 30,
+             section_bytes(cfg_of(dw, max_tokens=dw.T, n_layers=N_ROT), dw)]
     if not args.no_prefill or args.prefill_only:
         sizes.append(section_bytes(cfg_of(pw0, max_tokens=pw0.T), pw0))
     if not args.no_ep_share:
@@ -571,19 +621,27 @@ def main():
                           "kernels_ms": {k: v["ms_per_launch"] for k, v in pkern.items()}}),
               flush=True)
         player.close()
+        del player, px
+        pool_release()
         return
 
     wl = mi.WORKLOADS["decode"]
-    log("setup decode layer (16 experts, 6.3 GB) ...")
-    layer, x = setup_layer(wl, max_tokens=wl.T)
+    log(f"setup decode layers ({N_ROT} seeded copies of the 16-expert layer, "
+        f"{N_ROT * 6.34:.0f} GB) ...")
+    layer, x = setup_rotation(wl, N_ROT, max_tokens=wl.T)
     log("timing decode ...")
     # the step time comes from a region without per-kernel events (each event
-    # pair adds a few microseconds to a ~0.26 ms step); a second timed region
-    # of the same steps brackets every kernel with events for the roofline
-    ms, _, rt, _ = time_layer(layer, x, args.steps, args.warmup, kernel_events=False)
-    ms_ev, kern, _, dropped = time_layer(layer, x, args.steps, 0, kernel_events=True)
+    # pair adds a few microseconds to a ~0.24 ms step); a second timed region
+    # of the same steps brackets every kernel with events for the roofline.
+    # Step i runs layer i % N_ROT.
+    ms, _, rt, _ = time_layer(layer, x, args.steps, args.warmup, kernel_events=False, n_rot=N_ROT)
+    ms_ev, kern, _, dropped = time_layer(layer, x, args.steps, 0, kernel_events=True, n_rot=N_ROT)
+    touched_per_layer = []
+    for li in range(N_ROT):
+        rtl = layer.routing_tensors(layer.route(li, x))
+        touched_per_layer.append(int((rtl["counts"] > 0).sum()))
     log(f"decode ms/step {ms:.4f} (with per-kernel events {ms_ev:.4f})")
-    touched = int((rt["counts"] > 0).sum())
+    touched = sum(touched_per_layer) / N_ROT
     expert_bytes = 3 * wl.d * wl.f * 2
     gu_unit = 2 * wl.d * wl.f * 2                     # one touched expert's gate+up
     layer_bytes = touched * expert_bytes + wl.d * wl.E * 4 + 2 * wl.T * wl.d * 2
@@ -669,6 +727,7 @@ def main():
         "hbm_read_ceiling_gbs": read_gbs,
         "hbm_frac_of_ceiling": hbm_gbs / read_gbs,
         "touched_experts": touched,
+        "decode_rotation_layers": N_ROT,
         "roofline": {"bound": "hbm", "kernel": "decode_gateup", "achieved": gu_gbs,
                      "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": gu_gbs / HBM_PEAK_GBS,
                      "traffic": measured_traffic(), "algorithmic_bytes": gu_bytes},
@@ -681,6 +740,7 @@ def main():
         "stack": stack,
         "perf_model": model,
     }
+    pool_release()
     print(json.dumps(out), flush=True)
 
 

@@ -69,6 +69,11 @@ typedef enum {
     MOE_E_HIP = -6       /* a HIP runtime call failed */
 } moe_status;
 
+/* Configuration flags (moe_config.flags). */
+#define MOE_PARTIAL_F32 0x1 /* moe_forward writes y as fp32 [T, d], unrounded
+                               (an expert-parallel share's partial sum that a
+                               cross-device all-reduce adds, Sec. 4.3) */
+
 /* Layer configuration.
  *   d_model, ffn_dim : D_embed and D_ffn (Table tab:vars: 6144 and 10752).
  *                      d_model must be a multiple of 256, ffn_dim of 128.
@@ -82,7 +87,7 @@ typedef enum {
  *                      max_tokens * d_model * 2 must stay below 2^31.
  *   d_model * ffn_dim * 4 (one expert's packed gate/up bytes) must stay
  *                      below 2^31.
- *   flags            : must be 0. */
+ *   flags            : 0 or MOE_PARTIAL_F32; any other bit is rejected. */
 typedef struct {
     int32_t d_model, ffn_dim, n_experts, top_k;
     int32_t expert_begin, n_local_experts;
@@ -114,13 +119,19 @@ typedef struct {
 
 /* Bytes of the persistent weight arena / workspace for cfg (0 if cfg is
  * invalid).  The arena holds, per layer, the router (fp32) and every local
- * expert's three matrices repacked into the kernels' tiled layout. */
+ * expert's three matrices repacked into the kernels' tiled layout (Sec. 4.1:
+ * the weights are stacked once into one persistent array). */
 MOE_API size_t moe_weight_bytes(const moe_config *cfg);
 MOE_API size_t moe_workspace_bytes(const moe_config *cfg);
 
-/* Validates cfg, records the caller-allocated device buffers (sizes from the
- * functions above; they must stay allocated and unmoved until moe_destroy)
- * and returns a new context in *out.  Allocates only the host-side context.
+/* Sec. 4.1 (prestacking: buffers set up once, so that no call afterwards
+ * pays for memory management) and Sec. 3.1 / Sec. 4.3 (a node holds a range
+ * of the experts).  Validates cfg, records the caller-allocated device
+ * buffers (sizes from the functions above, both 256-byte aligned; they must
+ * stay allocated and unmoved until moe_destroy) and returns a new context in
+ * *out.  Allocates only the host-side context.  Errors: MOE_E_SHAPE for an
+ * invalid cfg, MOE_E_ARG for a NULL buffer or out, MOE_E_ALIGN; *out is then
+ * NULL and moe_last_error(NULL) holds the reason.
  * The weight stream is sensitive to where the arena lands: measured, an arena
  * placed in memory that earlier allocations had used and freed streams 2-4 %
  * slower than one carved from a single large allocation made up front. */
@@ -139,34 +150,71 @@ MOE_API moe_status moe_load_expert(moe_ctx *ctx, int32_t layer, int32_t expert,
                            const uint16_t *down, int32_t src_on_device,
                            moe_stream_t stream);
 
-/* Loads one layer's router: wr fp32 [d, E] row-major, bias fp32 [E] or NULL
- * (no bias).  Same src_on_device rule as moe_load_expert. */
+/* Sec. 3.1 and Sec. 4.3 (the router decides where each token goes; every
+ * node holds a full copy of it).  Loads one layer's router: wr fp32 [d, E]
+ * row-major, bias fp32 [E] or NULL (no bias).  Same src_on_device rule as
+ * moe_load_expert.  A routing returned for this layer before the call is no
+ * longer accepted by moe_forward. */
 MOE_API moe_status moe_load_router(moe_ctx *ctx, int32_t layer, const float *wr,
                            const float *bias, int32_t src_on_device,
                            moe_stream_t stream);
 
-/* Router, selection and permutation for T tokens of x (bf16 [T, d]).  If
+/* Sec. 2.1 (the router selects 4 of the 16 experts per token), Sec. 3.1
+ * (its output decides which experts, and so which nodes, receive a token).
+ * Router, selection and permutation for T tokens of x (bf16 [T, d]).  If
  * logits_in (fp32 [T, E], device) is not NULL it is routed as given and the
- * router product is skipped.  On MOE_OK, *out describes the routing (views
- * into the workspace).  T == 0 is a no-op that reports an empty routing. */
+ * router product is skipped (x may then be NULL).  On MOE_OK, *out describes
+ * the routing (views into the workspace).  T == 0 is a no-op that reports an
+ * empty routing.  Errors: MOE_E_ARG (layer, T < 0, NULL out or x),
+ * MOE_E_CAPACITY (T > max_tokens), MOE_E_STATE (router not loaded),
+ * MOE_E_ALIGN. */
 MOE_API moe_status moe_route(moe_ctx *ctx, int32_t layer, const uint16_t *x, int32_t T,
                      const float *logits_in, moe_routing *out,
                      moe_stream_t stream);
 
-/* The layer: y (bf16 [T, d]) = weighted sum of the local selected experts.
- * If r is NULL the routing is computed first (as moe_route with NULL
- * logits_in); otherwise r must be the routing that the last moe_route on this
- * context returned, for the same layer, x and T.  For an expert-parallel
- * share, y is the partial sum of the local slots (zero rows for tokens with
- * no local slot).  Requires the layer's router and local experts loaded. */
+/* Sec. 2.1 (the selected experts are GLU FFNs, Table tab:vars (e)), Sec. 2.2
+ * (their outputs are combined by a weighted sum), Sec. 4.3 (a node computes
+ * only its local experts and returns their partial sum).
+ * The layer: y = weighted sum of the local selected experts, bf16 [T, d], or
+ * fp32 [T, d] (unrounded) when the config has MOE_PARTIAL_F32.  If r is NULL
+ * the routing is computed first (as moe_route with NULL logits_in);
+ * otherwise r must be the routing that the last moe_route on this context
+ * returned, for the same layer and T, and -- if it was computed from x rather
+ * than given logits -- the same x; a forward with internal routing, a stack
+ * forward or a moe_load_router of that layer in between invalidates it
+ * (MOE_E_STATE).  For an expert-parallel share, y is the partial sum of the
+ * local slots (zero rows for tokens with no local slot).  Requires the
+ * layer's router and local experts loaded (MOE_E_STATE otherwise). */
 MOE_API moe_status moe_forward(moe_ctx *ctx, int32_t layer, const uint16_t *x,
-                       int32_t T, const moe_routing *r, uint16_t *y,
+                       int32_t T, const moe_routing *r, void *y,
                        moe_stream_t stream);
 
-/* All n_layers layers in order on T tokens, in place: for each layer l,
- * x = bf16(x + layer_l(x)).  x_inout is bf16 [T, d]. */
+/* Sec. 4.1 (all layers' experts resident in one prestacked array, indexed
+ * per layer) and Sec. 2.1 (one MoE FFN per decoder layer).  All n_layers
+ * layers in order on T tokens, in place: for each layer l,
+ * x = bf16(x + layer_l(x)), always bf16 (MOE_PARTIAL_F32 does not apply).
+ * x_inout is bf16 [T, d].  Requires every layer loaded (MOE_E_STATE). */
 MOE_API moe_status moe_forward_stack(moe_ctx *ctx, uint16_t *x_inout, int32_t T,
                              moe_stream_t stream);
+
+/* Workspace map for a caller that owns the workspace and wants to inspect or
+ * guard its parts: region i (moe_ws_region order) starts offset[i] bytes
+ * into the workspace and holds bytes[i] bytes; the gaps between regions
+ * (alignment padding) are never written.  Fills min(n, MOE_WS_COUNT)
+ * entries and returns MOE_WS_COUNT, or 0 if cfg is invalid. */
+typedef enum {
+    MOE_WS_ROUTE_PARTIALS = 0, /* fp64 partial logits of the small-T router */
+    MOE_WS_LOGITS, MOE_WS_TOPK_IDX, MOE_WS_TOPK_W, MOE_WS_COUNTS, MOE_WS_OFFSETS,
+    MOE_WS_PAIR_ROW, MOE_WS_ROW_TOKEN,
+    MOE_WS_ACTIVE,             /* int32 [1 + E]: #active local experts, their ids */
+    MOE_WS_TILES,              /* int32 [max_tiles][2]: GEMM token tiles */
+    MOE_WS_N_TILES,            /* int32 [1] */
+    MOE_WS_H,                  /* bf16 [rows_max, f] */
+    MOE_WS_O,                  /* fp32 [rows_max, d] */
+    MOE_WS_COUNT
+} moe_ws_region;
+MOE_API int32_t moe_workspace_map(const moe_config *cfg, uint64_t *offset, uint64_t *bytes,
+                                  int32_t n);
 
 /* Introspection for tests: device pointers to the intermediates of the last
  * forward on ctx, valid until the next forward.  h: bf16 [rows, f], the

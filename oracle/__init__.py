@@ -40,11 +40,13 @@ def lib():
         L.oracle_permutation.argtypes = [_i, _i, _i, _i, _i, _p, _p, _p, _p, _p]
         L.oracle_expert_glu.argtypes = [_i, _i, _i, _p, _p, _p, _p, _p, _p]
         L.oracle_layer_with_routing.argtypes = [_i] * 7 + [_p] * 8
+        L.oracle_layer_with_routing_ex.argtypes = [_i] * 7 + [_p] * 6 + [_i] + [_p] * 3
         L.oracle_layer.argtypes = [_i] * 7 + [_p] * 11
         L.oracle_layer_dense.argtypes = [_i] * 5 + [_p] * 7
         L.oracle_residual_add.argtypes = [_p, _p, _p, ctypes.c_int64]
         for fn in ("oracle_router_logits", "oracle_route_from_logits", "oracle_permutation",
-                   "oracle_expert_glu", "oracle_layer_with_routing", "oracle_layer",
+                   "oracle_expert_glu", "oracle_layer_with_routing",
+                   "oracle_layer_with_routing_ex", "oracle_layer",
                    "oracle_layer_dense"):
             getattr(L, fn).restype = ctypes.c_int
         _LIB = L
@@ -163,6 +165,35 @@ def layer_with_routing(x, idx, w, gates, ups, downs, e_begin: int = 0, n_local: 
                                            y64.ctypes.data, y16.ctypes.data),
            "layer_with_routing")
     return y64, y16
+
+
+def layer_with_routing_ex(x, idx, w, gates, ups, downs, e_begin: int = 0, n_local: int = 0,
+                          round_h: bool = True, want_hb: bool = False):
+    """layer_with_routing with the per-pair H and the exact form.
+
+    Returns (y64, y16, hb): hb is bf16 bits [T, k, f] (pair (t, j)'s H when
+    its expert is local, 0 otherwise) or None.  round_h=False is the
+    information-only exact form: H is not rounded before the down
+    projection, so y64 carries no intermediate rounding at all."""
+    x, px = _c(x, np.uint16)
+    idx, pi = _c(idx, np.int32)
+    w, pw = _c(w, np.float64)
+    T, d = x.shape
+    k = idx.shape[1]
+    E = len(gates)
+    f = next(g for g in gates if g is not None).shape[1]
+    nl = n_local or E
+    pg, kg = _ptr_array(gates, E)
+    pu, ku = _ptr_array(ups, E)
+    pd, kd = _ptr_array(downs, E)
+    y64 = np.empty((T, d), dtype=np.float64)
+    y16 = np.empty((T, d), dtype=np.uint16)
+    hb = np.zeros((T, k, f), dtype=np.uint16) if want_hb else None
+    _check(lib().oracle_layer_with_routing_ex(T, d, f, E, k, e_begin, nl, px, pi, pw, pg, pu, pd,
+                                              int(round_h), y64.ctypes.data, y16.ctypes.data,
+                                              hb.ctypes.data if want_hb else None),
+           "layer_with_routing_ex")
+    return y64, y16, hb
 
 
 def layer(x, wr, bias, gates, ups, downs, k: int, e_begin: int = 0, n_local: int = 0):

@@ -225,10 +225,12 @@ static double silu(double z)
 
 /* One expert on m rows (R4, R5):
  *   g = x w1, u = x v1 (fp64), h = silu(g) * u, hb = bf16(h), o = hb w2 (fp64).
- * xrows bf16 [m,d]; hb_out bf16 [m,f] (may be NULL); o_out fp64 [m,d]. */
-int oracle_expert_glu(int m, int d, int f, const uint16_t *xrows,
+ * xrows bf16 [m,d]; hb_out bf16 [m,f] (may be NULL); o_out fp64 [m,d].
+ * round_h = 0 is the information-only exact form: the down projection takes
+ * h itself instead of hb (hb_out still receives bf16(h)). */
+static int expert_glu(int m, int d, int f, const uint16_t *xrows,
                       const uint16_t *gate, const uint16_t *up,
-                      const uint16_t *down, uint16_t *hb_out, double *o_out)
+                      const uint16_t *down, int round_h, uint16_t *hb_out, double *o_out)
 {
     if (m < 0 || d <= 0 || f <= 0 || (m > 0 && (!xrows || !gate || !up || !down || !o_out)))
         return ORC_EARG;
@@ -259,8 +261,9 @@ int oracle_expert_glu(int m, int d, int f, const uint16_t *xrows,
                 }
             }
             for (int n = n0; n < n1; ++n) {
-                uint16_t hbits = oracle_bf16_from_f64(silu(g[n]) * u[n]);
-                hb[n] = oracle_f64_from_bf16(hbits);
+                double h = silu(g[n]) * u[n];
+                uint16_t hbits = oracle_bf16_from_f64(h);
+                hb[n] = round_h ? oracle_f64_from_bf16(hbits) : h;
                 if (hb_out)
                     hb_out[(int64_t)r * f + n] = hbits;
             }
@@ -284,18 +287,28 @@ int oracle_expert_glu(int m, int d, int f, const uint16_t *xrows,
     return ORC_OK;
 }
 
+int oracle_expert_glu(int m, int d, int f, const uint16_t *xrows,
+                      const uint16_t *gate, const uint16_t *up,
+                      const uint16_t *down, uint16_t *hb_out, double *o_out)
+{
+    return expert_glu(m, d, f, xrows, gate, up, down, 1, hb_out, o_out);
+}
+
 /* ---------------------------------------------------------------- layer -- */
 
 /* Steps 4-5 of the layer on a given routing (R6, R7):
  *   y[t] = bf16( sum over slots j of t whose expert is local: w[t,j] * o_j ).
- * y64 (fp64 [T,d], before the final rounding) and y16 (bf16 [T,d]) may each
- * be NULL. */
-int oracle_layer_with_routing(int T, int d, int f, int E, int k, int e_begin,
-                              int n_local, const uint16_t *x, const int32_t *idx,
-                              const double *w, const uint16_t *const *gate,
-                              const uint16_t *const *up,
-                              const uint16_t *const *down, double *y64,
-                              uint16_t *y16)
+ * y64 (fp64 [T,d], before the final rounding), y16 (bf16 [T,d]) and hb
+ * (bf16 [T*k, f]: row t*k+j receives pair (t,j)'s hb when its expert is
+ * local; other rows are left as they are) may each be NULL.  round_h = 0 is
+ * the information-only exact form (no rounding of H; y64 is then the layer
+ * with no intermediate rounding at all). */
+int oracle_layer_with_routing_ex(int T, int d, int f, int E, int k, int e_begin,
+                                 int n_local, const uint16_t *x, const int32_t *idx,
+                                 const double *w, const uint16_t *const *gate,
+                                 const uint16_t *const *up,
+                                 const uint16_t *const *down, int round_h, double *y64,
+                                 uint16_t *y16, uint16_t *hb)
 {
     if (T < 0 || d <= 0 || f <= 0 || E <= 0 || k <= 0 || k > E || e_begin < 0 ||
         n_local <= 0 || e_begin + n_local > E)
@@ -316,8 +329,8 @@ int oracle_layer_with_routing(int T, int d, int f, int E, int k, int e_begin,
             if (e < e_begin || e >= e_begin + n_local)
                 continue;
             if (!gate[e] || !up[e] || !down[e]) { rc = ORC_EARG; break; }
-            rc = oracle_expert_glu(1, d, f, x + (int64_t)t * d, gate[e], up[e],
-                                   down[e], NULL, o);
+            rc = expert_glu(1, d, f, x + (int64_t)t * d, gate[e], up[e], down[e], round_h,
+                            hb ? hb + ((int64_t)t * k + j) * f : NULL, o);
             if (rc != ORC_OK)
                 break;
             double wj = w[(int64_t)t * k + j];
@@ -333,6 +346,17 @@ int oracle_layer_with_routing(int T, int d, int f, int E, int k, int e_begin,
     }
     free(o); free(acc);
     return rc;
+}
+
+int oracle_layer_with_routing(int T, int d, int f, int E, int k, int e_begin,
+                              int n_local, const uint16_t *x, const int32_t *idx,
+                              const double *w, const uint16_t *const *gate,
+                              const uint16_t *const *up,
+                              const uint16_t *const *down, double *y64,
+                              uint16_t *y16)
+{
+    return oracle_layer_with_routing_ex(T, d, f, E, k, e_begin, n_local, x, idx, w, gate, up,
+                                        down, 1, y64, y16, NULL);
 }
 
 /* The whole layer: router logits, selection and weights, then the experts

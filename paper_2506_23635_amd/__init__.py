@@ -16,11 +16,15 @@ PKG_DIR = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(PKG_DIR, "libmoe.so")
 
 MOE_OK = 0
+MOE_PARTIAL_F32 = 0x1   # moe_config.flags: y of moe_forward is fp32 [T, d]
 DIAG_MAX_WG = 512    # MOE_DIAG_MAX_WG of include/moe.h
+WS_REGIONS = ["route_partials", "logits", "topk_idx", "topk_w", "counts", "offsets", "pair_row",
+              "row_token", "active", "tiles", "n_tiles", "h", "o"]   # moe_ws_region order
 STATUS_NAMES = {0: "MOE_OK", -1: "MOE_E_ARG", -2: "MOE_E_SHAPE", -3: "MOE_E_ALIGN",
                 -4: "MOE_E_CAPACITY", -5: "MOE_E_STATE", -6: "MOE_E_HIP"}
 
-EXPORTED = ["moe_weight_bytes", "moe_workspace_bytes", "moe_init", "moe_load_expert",
+EXPORTED = ["moe_weight_bytes", "moe_workspace_bytes", "moe_workspace_map", "moe_init",
+            "moe_load_expert",
             "moe_load_router", "moe_route", "moe_forward", "moe_forward_stack",
             "moe_intermediates", "moe_profile_enable", "moe_profile_read", "moe_destroy",
             "moe_last_error", "moe_status_string", "moe_diag_stream_read"]
@@ -70,6 +74,8 @@ def lib():
         L.moe_weight_bytes.restype = ctypes.c_size_t
         L.moe_workspace_bytes.argtypes = [cfgp]
         L.moe_workspace_bytes.restype = ctypes.c_size_t
+        L.moe_workspace_map.argtypes = [cfgp, P, P, I]
+        L.moe_workspace_map.restype = ctypes.c_int32
         L.moe_init.argtypes = [cfgp, P, P, ctypes.POINTER(P)]
         L.moe_load_expert.argtypes = [P, I, I, P, P, P, I, P]
         L.moe_load_router.argtypes = [P, I, P, P, I, P]
@@ -112,6 +118,17 @@ def moe_weight_bytes(cfg: MoeConfig) -> int:
 
 def moe_workspace_bytes(cfg: MoeConfig) -> int:
     return int(lib().moe_workspace_bytes(ctypes.byref(cfg)))
+
+
+def moe_workspace_map(cfg: MoeConfig) -> dict:
+    """{region name: (byte offset, bytes)} of the workspace for cfg."""
+    n = len(WS_REGIONS)
+    off = (ctypes.c_uint64 * n)()
+    nb = (ctypes.c_uint64 * n)()
+    got = lib().moe_workspace_map(ctypes.byref(cfg), off, nb, n)
+    if got != n:
+        raise MoeError(-2, "invalid config" if got == 0 else f"{got} regions, expected {n}")
+    return {name: (int(off[i]), int(nb[i])) for i, name in enumerate(WS_REGIONS)}
 
 
 def moe_init(cfg: MoeConfig, arena_ptr: int, workspace_ptr: int) -> int:
@@ -292,10 +309,12 @@ class MoeLayer:
         return moe_route(self.ctx, layer, xp, T, lp, self.stream)
 
     def forward(self, layer, x, y, routing=None, T=None):
+        """y: bf16 [T, d], or fp32 [T, d] when the config has MOE_PARTIAL_F32."""
         T = self._tokens(x, T)
         n, bf = T * self.cfg.d_model, _bf16_types(self.torch)
+        ytypes = (self.torch.float32,) if self.cfg.flags & MOE_PARTIAL_F32 else bf
         moe_forward(self.ctx, layer, _tensor_ptr(x, "x", n, bf, self.device), T, routing,
-                    _tensor_ptr(y, "y", n, bf, self.device), self.stream)
+                    _tensor_ptr(y, "y", n, ytypes, self.device), self.stream)
 
     def forward_stack(self, x, T=None):
         T = self._tokens(x, T)

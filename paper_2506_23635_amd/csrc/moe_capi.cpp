@@ -32,6 +32,7 @@ struct Layout {
     // workspace
     size_t dpart_off, logits_off, idx_off, w_off, counts_off, offsets_off, pair_row_off,
         row_token_off, active_off, tiles_off, n_tiles_off, h_off, o_off, ws_bytes;
+    size_t region_off[MOE_WS_COUNT], region_bytes[MOE_WS_COUNT];   // moe_workspace_map
     int rows_max, max_tiles;
 };
 
@@ -51,7 +52,7 @@ const char* check_config(const moe_config* c)
         return "max_tokens * d_model * 2 must stay below 2^31 (32-bit gather offsets)";
     if ((int64_t)c->d_model * c->ffn_dim * 4 > INT32_MAX)
         return "d_model * ffn_dim * 4 (one expert's gate/up slab) must stay below 2^31";
-    if (c->flags != 0) return "flags must be 0";
+    if (c->flags & ~MOE_PARTIAL_F32) return "flags: only MOE_PARTIAL_F32 is defined";
     return nullptr;
 }
 
@@ -74,20 +75,26 @@ Layout make_layout(const moe_config* c)
     const int tile_rows = moe_prefill_tile_rows();
     L.max_tiles = (int)((L.rows_max + tile_rows - 1) / tile_rows + nl);
     size_t off = 0;
-    auto take = [&](size_t bytes) { size_t o = off; off = align_up(off + bytes, kAlign); return o; };
-    L.dpart_off = take((size_t)moe_route_decode_wgs(c->d_model) * 16 * 16 * 8);
-    L.logits_off = take(Tm * E * 4);
-    L.idx_off = take(Tm * k * 4);
-    L.w_off = take(Tm * k * 4);
-    L.counts_off = take(E * 4);
-    L.offsets_off = take((E + 1) * 4);
-    L.pair_row_off = take(Tm * k * 4);
-    L.row_token_off = take(Tm * k * 4);
-    L.active_off = take((E + 1) * 4);
-    L.tiles_off = take((size_t)L.max_tiles * 2 * 4);
-    L.n_tiles_off = take(4);
-    L.h_off = take((size_t)L.rows_max * f * 2);
-    L.o_off = take((size_t)L.rows_max * d * 4);
+    auto take = [&](int region, size_t bytes) {
+        size_t o = off;
+        off = align_up(off + bytes, kAlign);
+        L.region_off[region] = o;
+        L.region_bytes[region] = bytes;
+        return o;
+    };
+    L.dpart_off = take(MOE_WS_ROUTE_PARTIALS, (size_t)moe_route_decode_wgs(c->d_model) * 16 * 16 * 8);
+    L.logits_off = take(MOE_WS_LOGITS, Tm * E * 4);
+    L.idx_off = take(MOE_WS_TOPK_IDX, Tm * k * 4);
+    L.w_off = take(MOE_WS_TOPK_W, Tm * k * 4);
+    L.counts_off = take(MOE_WS_COUNTS, E * 4);
+    L.offsets_off = take(MOE_WS_OFFSETS, (E + 1) * 4);
+    L.pair_row_off = take(MOE_WS_PAIR_ROW, Tm * k * 4);
+    L.row_token_off = take(MOE_WS_ROW_TOKEN, Tm * k * 4);
+    L.active_off = take(MOE_WS_ACTIVE, (E + 1) * 4);
+    L.tiles_off = take(MOE_WS_TILES, (size_t)L.max_tiles * 2 * 4);
+    L.n_tiles_off = take(MOE_WS_N_TILES, 4);
+    L.h_off = take(MOE_WS_H, (size_t)L.rows_max * f * 2);
+    L.o_off = take(MOE_WS_O, (size_t)L.rows_max * d * 4);
     L.ws_bytes = off;
     return L;
 }
@@ -105,16 +112,16 @@ struct moe_ctx {
     std::vector<uint8_t> has_bias;        // [n_layers]
     std::vector<uint8_t> expert_loaded;   // [n_layers * n_local]
     moe::RouteView rv;
-    bool gemm_lds_set;      // dynamic-LDS limit raised for the GEMM kernels
     // per-kernel timing (moe_profile_*): an event pair around each launch
     bool prof_on;
     std::vector<hipEvent_t> prof_events;   // 2 per launch slot
     std::vector<int> prof_kinds;           // kind of each recorded launch
     int64_t prof_dropped;
-    // last routing
+    // the routing that the last moe_route returned (moe_forward accepts it
+    // while nothing has overwritten or outdated it)
     bool route_valid;
     int route_layer, route_T;
-    const uint16_t* route_x;
+    const uint16_t* route_x;   // the x it was computed from; NULL for given logits
     std::string err;
 };
 
@@ -198,10 +205,6 @@ moe_status do_route(moe_ctx* ctx, int layer, const uint16_t* x, int T, const flo
         });
         if (e != hipSuccess) return hip_fail(ctx, e, "route kernel launch");
     }
-    ctx->route_valid = true;
-    ctx->route_layer = layer;
-    ctx->route_T = T;
-    ctx->route_x = x;
     return MOE_OK;
 }
 
@@ -261,11 +264,6 @@ moe_status run_experts(moe_ctx* ctx, int layer, const uint16_t* x, int T, hipStr
         a.f = c.ffn_dim;
         a.e_begin = c.expert_begin;
         a.T = T;
-        if (!ctx->gemm_lds_set) {
-            e = moe_prefill_set_lds_limit();
-            if (e != hipSuccess) return hip_fail(ctx, e, "GEMM kernel LDS attribute");
-            ctx->gemm_lds_set = true;
-        }
         const int tile_rows = moe_prefill_tile_rows();
         const int kl = std::min(c.top_k, c.n_local_experts);
         a.max_tiles = (T * kl + tile_rows - 1) / tile_rows + c.n_local_experts;
@@ -308,6 +306,17 @@ size_t moe_workspace_bytes(const moe_config* cfg)
     return make_layout(cfg).ws_bytes;
 }
 
+int32_t moe_workspace_map(const moe_config* cfg, uint64_t* offset, uint64_t* bytes, int32_t n)
+{
+    if (check_config(cfg)) return 0;
+    const Layout L = make_layout(cfg);
+    for (int i = 0; i < n && i < MOE_WS_COUNT; ++i) {
+        if (offset) offset[i] = L.region_off[i];
+        if (bytes) bytes[i] = L.region_bytes[i];
+    }
+    return MOE_WS_COUNT;
+}
+
 moe_status moe_init(const moe_config* cfg, void* weight_arena, void* workspace, moe_ctx** out)
 {
     if (!out) return fail(nullptr, MOE_E_ARG, "out is NULL");
@@ -337,7 +346,9 @@ moe_status moe_init(const moe_config* cfg, void* weight_arena, void* workspace, 
     c->rv.tiles = reinterpret_cast<int32_t*>(w + c->L.tiles_off);
     c->rv.n_tiles = reinterpret_cast<int32_t*>(w + c->L.n_tiles_off);
     c->route_valid = false;
-    c->gemm_lds_set = false;
+    c->route_layer = -1;
+    c->route_T = 0;
+    c->route_x = nullptr;
     c->prof_on = false;
     c->prof_dropped = 0;
     *out = c;
@@ -394,6 +405,7 @@ moe_status moe_load_router(moe_ctx* ctx, int32_t layer, const float* wr, const f
     const moe_config& c = ctx->cfg;
     if (layer < 0 || layer >= c.n_layers) return fail(ctx, MOE_E_ARG, "layer out of range");
     if (!wr) return fail(ctx, MOE_E_ARG, "router weight is NULL");
+    if (ctx->route_layer == layer) ctx->route_valid = false;
     uint8_t* lb = layer_base(ctx, layer);
     hipStream_t s = static_cast<hipStream_t>(stream);
     const int d = c.d_model, E = c.n_experts;
@@ -420,6 +432,7 @@ moe_status moe_load_router(moe_ctx* ctx, int32_t layer, const float* wr, const f
         if (e == hipSuccess) e = hipStreamSynchronize(s);
     }
     if (e != hipSuccess) return hip_fail(ctx, e, "router load");
+    if (ctx->route_layer == layer) ctx->route_valid = false;   // routed with the old router
     ctx->router_loaded[layer] = 1;
     ctx->has_bias[layer] = bias ? 1 : 0;
     return MOE_OK;
@@ -447,12 +460,16 @@ moe_status moe_route(moe_ctx* ctx, int32_t layer, const uint16_t* x, int32_t T,
     }
     moe_status st = do_route(ctx, layer, x, T, logits_in, static_cast<hipStream_t>(stream));
     if (st != MOE_OK) return st;
+    ctx->route_valid = true;
+    ctx->route_layer = layer;
+    ctx->route_T = T;
+    ctx->route_x = logits_in ? nullptr : x;
     fill_routing(ctx, layer, T, out);
     return MOE_OK;
 }
 
 moe_status moe_forward(moe_ctx* ctx, int32_t layer, const uint16_t* x, int32_t T,
-                       const moe_routing* r, uint16_t* y, moe_stream_t stream)
+                       const moe_routing* r, void* y, moe_stream_t stream)
 {
     if (!ctx) return MOE_E_ARG;
     if (T < 0) return fail(ctx, MOE_E_ARG, "T is negative");
@@ -466,17 +483,23 @@ moe_status moe_forward(moe_ctx* ctx, int32_t layer, const uint16_t* x, int32_t T
     if (r) {
         if (!ctx->route_valid || r->T != T || r->layer != layer || r->logits != ctx->rv.logits ||
             ctx->route_T != T || ctx->route_layer != layer)
-            return fail(ctx, MOE_E_STATE, "routing does not belong to the last moe_route of this layer and T");
+            return fail(ctx, MOE_E_STATE,
+                        "routing is not the current result of the last moe_route for this layer and T");
+        if (ctx->route_x && ctx->route_x != x)
+            return fail(ctx, MOE_E_STATE, "routing was computed from a different x");
     } else {
+        ctx->route_valid = false;   // the views are about to be overwritten
         st = do_route(ctx, layer, x, T, nullptr, s);
         if (st != MOE_OK) return st;
     }
     st = run_experts(ctx, layer, x, T, s);
     if (st != MOE_OK) return st;
+    const bool f32_out = (ctx->cfg.flags & MOE_PARTIAL_F32) != 0;
     hipError_t e = timed(ctx, MOE_K_COMBINE, s, [&] {
         return moe_launch_combine(reinterpret_cast<const float*>(ctx->ws + ctx->L.o_off),
                                   ctx->rv.pair_row, ctx->rv.topk_w, T, ctx->cfg.d_model,
-                                  ctx->cfg.top_k, y, nullptr, s);
+                                  ctx->cfg.top_k, f32_out ? nullptr : static_cast<uint16_t*>(y),
+                                  f32_out ? static_cast<float*>(y) : nullptr, nullptr, s);
     });
     if (e != hipSuccess) return hip_fail(ctx, e, "combine kernel launch");
     return MOE_OK;
@@ -495,6 +518,7 @@ moe_status moe_forward_stack(moe_ctx* ctx, uint16_t* x_inout, int32_t T, moe_str
     if (!x_inout) return fail(ctx, MOE_E_ARG, "x is NULL");
     if (misaligned(x_inout)) return fail(ctx, MOE_E_ALIGN, "x must be 16-byte aligned");
     hipStream_t s = static_cast<hipStream_t>(stream);
+    ctx->route_valid = false;   // the routing views are overwritten layer by layer
     for (int l = 0; l < ctx->cfg.n_layers; ++l) {
         moe_status st = do_route(ctx, l, x_inout, T, nullptr, s);
         if (st != MOE_OK) return st;
@@ -503,7 +527,7 @@ moe_status moe_forward_stack(moe_ctx* ctx, uint16_t* x_inout, int32_t T, moe_str
         hipError_t e = timed(ctx, MOE_K_COMBINE, s, [&] {
             return moe_launch_combine(reinterpret_cast<const float*>(ctx->ws + ctx->L.o_off),
                                       ctx->rv.pair_row, ctx->rv.topk_w, T, ctx->cfg.d_model,
-                                      ctx->cfg.top_k, nullptr, x_inout, s);
+                                      ctx->cfg.top_k, nullptr, nullptr, x_inout, s);
         });
         if (e != hipSuccess) return hip_fail(ctx, e, "combine kernel launch");
     }

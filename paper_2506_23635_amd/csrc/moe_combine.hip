@@ -5,9 +5,16 @@
 //
 // y[t, n] = bf16( sum over slots j of t with a local expert: w[t,j] * O[row(t,j), n] )
 // The slots are summed in slot order in fp32 by the one thread that owns the
-// element, so the result is deterministic (no atomics).  With a residual the
-// kernel instead writes x[t, n] = bf16(x[t, n] + y[t, n]) in place; the sum of
-// two bf16 values is exact in fp64, so that is a single rounding.
+// element, so the result is deterministic (no atomics).  With y32 set the
+// unrounded fp32 sums are written instead (an expert-parallel share's partial
+// for a later cross-device reduction).  With a residual the kernel instead
+// writes x[t, n] = bf16(x[t, n] + y[t, n]) in place.
+//
+// The residual sum is one correct rounding although it is formed in fp32: two
+// bf16 values whose exponents differ by at most 15 add exactly in fp32's 24
+// bits; with a larger gap the smaller one is below 2^-15 of the larger, less
+// than half a bf16 step, so both the exact sum and its fp32 rounding round
+// to the larger value.
 #include "moe_common.h"
 
 namespace moe {
@@ -16,6 +23,7 @@ __global__ __launch_bounds__(256) void combine_kernel(const float* __restrict__ 
                                                       const int32_t* __restrict__ pair_row,
                                                       const float* __restrict__ topk_w, int T,
                                                       int d, int k, uint16_t* __restrict__ y,
+                                                      float* __restrict__ y32,
                                                       uint16_t* __restrict__ x_residual)
 {
     const int groups = d / 8;
@@ -44,12 +52,15 @@ __global__ __launch_bounds__(256) void combine_kernel(const float* __restrict__ 
             for (int h = 0; h < 2; ++h) {
                 const uint16_t xb = (uint16_t)(xv[i] >> (16 * h));
                 const uint16_t yb = f32_to_bf16(acc[2 * i + h]);
-                const double s = (double)bf16_to_f32(xb) + (double)bf16_to_f32(yb);
-                (h ? hi : lo) = f64_to_bf16(s);
+                (h ? hi : lo) = f32_to_bf16(bf16_to_f32(xb) + bf16_to_f32(yb));
             }
             out[i] = lo | (hi << 16);
         }
         *reinterpret_cast<u32x4_t*>(x_residual + (int64_t)t * d + n) = out;
+    } else if (y32) {
+        float4* py = reinterpret_cast<float4*>(y32 + (int64_t)t * d + n);
+        py[0] = make_float4(acc[0], acc[1], acc[2], acc[3]);
+        py[1] = make_float4(acc[4], acc[5], acc[6], acc[7]);
     } else {
 #pragma unroll
         for (int i = 0; i < 4; ++i)
@@ -63,11 +74,11 @@ __global__ __launch_bounds__(256) void combine_kernel(const float* __restrict__ 
 
 extern "C" hipError_t moe_launch_combine(const float* O, const int32_t* pair_row,
                                          const float* topk_w, int T, int d, int k, uint16_t* y,
-                                         uint16_t* x_residual, hipStream_t s)
+                                         float* y32, uint16_t* x_residual, hipStream_t s)
 {
     int64_t total = (int64_t)T * (d / 8);
     int grid = (int)((total + 255) / 256);
     hipLaunchKernelGGL(moe::combine_kernel, dim3(grid), dim3(256), 0, s, O, pair_row, topk_w, T,
-                       d, k, y, x_residual);
+                       d, k, y, y32, x_residual);
     return hipGetLastError();
 }

@@ -55,36 +55,6 @@ __device__ inline uint16_t f32_to_bf16(float v)
     return (uint16_t)(u >> 16);
 }
 
-// fp64 -> bf16, one rounding to nearest even, integer arithmetic on the bits.
-__device__ inline uint16_t f64_to_bf16(double v)
-{
-    uint64_t b = (uint64_t)__double_as_longlong(v);
-    uint16_t sign = (uint16_t)((b >> 48) & 0x8000u);
-    uint64_t a = b & 0x7FFFFFFFFFFFFFFFull;
-    if (a >= 0x7FF0000000000000ull)
-        return (uint16_t)(sign | (a == 0x7FF0000000000000ull ? 0x7F80u : 0x7FC0u));
-    int bexp = (int)(a >> 52);
-    if (bexp == 0)
-        return sign;
-    uint64_t mant = (a & 0x000FFFFFFFFFFFFFull) | 0x0010000000000000ull;
-    int e = bexp - 1023;
-    int qexp = (e < -126 ? -126 : e) - 7;
-    int shift = qexp - (bexp - 1075);
-    if (shift > 54)
-        return sign;
-    uint64_t q = mant >> shift;
-    uint64_t rem = mant & ((1ull << shift) - 1ull);
-    uint64_t half = 1ull << (shift - 1);
-    q += (rem > half || (rem == half && (q & 1ull))) ? 1ull : 0ull;
-    if (q >= 256ull) { q >>= 1; qexp += 1; }
-    if (q >= 128ull) {
-        int biased = qexp + 134;
-        if (biased >= 255) return (uint16_t)(sign | 0x7F80u);
-        return (uint16_t)(sign | (uint16_t)(biased << 7) | (uint16_t)(q & 127ull));
-    }
-    return (uint16_t)(sign | (uint16_t)q);
-}
-
 // silu(g) * u with an overflow-free logistic: for g << 0, exp(-g) -> inf and
 // g / inf -> -0, which is the limit.
 __device__ inline float silu_mul(float g, float u)
@@ -164,8 +134,8 @@ hipError_t moe_launch_decode_gateup(const moe::DecodeArgs* a, int n_slots, hipSt
 hipError_t moe_launch_decode_down(const moe::DecodeArgs* a, int n_slots, hipStream_t s);
 hipError_t moe_launch_gemm_gateup(const moe::GemmArgs* a, hipStream_t s);
 hipError_t moe_launch_gemm_down(const moe::GemmArgs* a, hipStream_t s);
-hipError_t moe_prefill_set_lds_limit();
 int moe_prefill_tile_rows();
 hipError_t moe_launch_combine(const float* O, const int32_t* pair_row, const float* topk_w, int T,
-                              int d, int k, uint16_t* y, uint16_t* x_residual, hipStream_t s);
+                              int d, int k, uint16_t* y, float* y32, uint16_t* x_residual,
+                              hipStream_t s);
 }

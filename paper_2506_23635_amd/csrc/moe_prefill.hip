@@ -261,7 +261,6 @@ __device__ __forceinline__ void tile_loop(const TileCtx& c, int n_pairs, uint8_t
 template <int kMode>
 __device__ __forceinline__ void process_tile(const GemmArgs& a, int ft, int tt, uint8_t* lds)
 {
-    const int M = kMode == kGateUp ? 2 * a.f : a.d;    // a multiple of 128
     const int e = a.tiles[2 * tt];
     const int row_start = a.tiles[2 * tt + 1];
     const int row_end = min(row_start + BN, a.offsets[e + 1]);
@@ -277,11 +276,9 @@ __device__ __forceinline__ void process_tile(const GemmArgs& a, int ft, int tt, 
     c.lane = threadIdx.x & 63;
     c.w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);   // wave-uniform, in an SGPR
     const int lane = c.lane, w = c.w;
-    // a wave past M (partial last feature tile) recomputes the last valid
-    // slab, keeping every load unconditional, and skips its stores
-    const bool wave_on = (uint64_t)ft * (BM / 16) + w * kWaveRt < (uint64_t)(M / 16);
-    const uint64_t rt0 =
-        wave_on ? (uint64_t)ft * (BM / 16) + w * kWaveRt : (uint64_t)(M / 16 - kWaveRt);
+    // M is a multiple of BM (the library requires d % 256 == 0 and
+    // f % 128 == 0), so every wave's 64-feature slab lies inside the matrix
+    const uint64_t rt0 = (uint64_t)ft * (BM / 16) + w * kWaveRt;
     // A: lane l of a 32 x 16 fragment reads row l%32 of the block (row tile
     // rt0 + 2 fb + (l%32)/16, granule row l%16) at K group l/32 of the step.
     // Buffer loads over the expert's slab (the library caps a slab below
@@ -344,7 +341,6 @@ __device__ __forceinline__ void process_tile(const GemmArgs& a, int ft, int tt, 
     // 8g + 4(l/32) + r in register 4g + r (g, r = 0..3).  A 32-row block is
     // row tiles (rt, rt + 1): for the gate/up GEMM that is 16 gate rows
     // (g = 0, 1) and the 16 up rows of the same features (g = 2, 3).
-    if (!wave_on) return;
     const int half = lane >> 5;
     const int jcol = lane & 31;
 #pragma unroll
@@ -381,8 +377,8 @@ template <int kMode>
 __global__ __launch_bounds__(kThreads) void gemm_kernel(GemmArgs a)
 {
     __shared__ __attribute__((aligned(16))) uint8_t lds[kRingB * B_STAGE_BYTES];
-    const int M = kMode == kGateUp ? 2 * a.f : a.d;
-    const int n_ftiles = (M + BM - 1) / BM;
+    const int M = kMode == kGateUp ? 2 * a.f : a.d;   // a multiple of BM
+    const int n_ftiles = M / BM;
     // XCD-aware numbering: hardware hands block b to XCD b % 8; each XCD
     // gets a contiguous run of logical tiles (feature tile major, token tile
     // fastest over the max_tiles slots the grid is sized for), so the
@@ -406,7 +402,7 @@ template <int kMode>
 static hipError_t launch_gemm(const moe::GemmArgs* a, hipStream_t s)
 {
     const int M = kMode == moe::kGateUp ? 2 * a->f : a->d;
-    const int n = (M + moe::BM - 1) / moe::BM * a->max_tiles;
+    const int n = M / moe::BM * a->max_tiles;
     const int grid = (n + moe::kXcds - 1) / moe::kXcds * moe::kXcds;
     hipLaunchKernelGGL((moe::gemm_kernel<kMode>), dim3(grid), dim3(moe::kThreads), 0, s, *a);
     return hipGetLastError();
@@ -422,4 +418,3 @@ extern "C" hipError_t moe_launch_gemm_down(const moe::GemmArgs* a, hipStream_t s
     return launch_gemm<moe::kDown>(a, s);
 }
 
-extern "C" hipError_t moe_prefill_set_lds_limit() { return hipSuccess; }

@@ -38,7 +38,7 @@ constexpr int kRouteWaves = kRouteThreads / kWave;
 constexpr int kMaxK = 8;
 
 template <int kMaxE>
-__device__ inline void select_token(const float* l, int E, int k, int* ids, float* w)
+__device__ __forceinline__ void select_token(const float* l, int E, int k, int* ids, float* w)
 {
     float lv[kMaxE];
 #pragma unroll
@@ -71,8 +71,9 @@ __device__ inline void select_token(const float* l, int E, int k, int* ids, floa
     for (int j = kMaxK; j < k; ++j) w[j] = w[j] * inv;
 }
 
-// selection of token t into the routing view
-__device__ inline void select_token_any(const float* l, int t, int E, int k, const RouteView& rv)
+// selection of token t into the routing view (inlined: as a call it spills
+// callee-saved registers to scratch)
+__device__ __forceinline__ void select_token_any(const float* l, int t, int E, int k, const RouteView& rv)
 {
     int* ids = rv.topk_idx + (int64_t)t * k;
     float* w = rv.topk_w + (int64_t)t * k;

@@ -59,7 +59,8 @@ def test_weight_bytes_formula():
 @pytest.mark.parametrize("bad", [dict(d_model=100), dict(d_model=0), dict(ffn_dim=96),
                                  dict(n_experts=0), dict(n_experts=65), dict(top_k=0),
                                  dict(top_k=17), dict(expert_begin=13, n_local_experts=4),
-                                 dict(n_layers=0), dict(max_tokens=0), dict(flags=1),
+                                 dict(n_layers=0), dict(max_tokens=0), dict(flags=2),
+                                 dict(flags=-1),
                                  dict(max_tokens=174763), dict(ffn_dim=87424)])
 def test_bad_configs_rejected(bad):
     # max_tokens 174763: x is then 2^31 bytes or more, past the GEMM's 32-bit gather offsets;
@@ -73,6 +74,39 @@ def test_bad_configs_rejected(bad):
     rc = moe.lib().moe_init(ctypes.byref(cfg), 4096, 8192, ctypes.byref(out))
     assert rc == E_SHAPE and out.value is None
     assert moe.moe_last_error(None)
+
+
+def test_partial_f32_flag_accepted():
+    cfg = dbrx(expert_begin=4, n_local_experts=4, flags=moe.MOE_PARTIAL_F32)
+    assert moe.moe_workspace_bytes(cfg) == moe.moe_workspace_bytes(dbrx(expert_begin=4,
+                                                                        n_local_experts=4))
+
+
+@pytest.mark.parametrize("kw", [dict(), dict(max_tokens=1), dict(expert_begin=4, n_local_experts=4),
+                                dict(d_model=256, ffn_dim=512, n_experts=8, top_k=2, max_tokens=300)])
+def test_workspace_map(kw):
+    """Regions in declaration order, each inside the workspace, none
+    overlapping, with the sizes the routing and intermediates need."""
+    cfg = dbrx(**kw)
+    m = moe.moe_workspace_map(cfg)
+    total = moe.moe_workspace_bytes(cfg)
+    assert list(m) == moe.WS_REGIONS
+    end = 0
+    for name in moe.WS_REGIONS:
+        off, n = m[name]
+        assert off >= end and off % 256 == 0 and n > 0, name
+        end = off + n
+    assert end <= total
+    T, E, k, d, f = cfg.max_tokens, cfg.n_experts, cfg.top_k, cfg.d_model, cfg.ffn_dim
+    rows = T * min(k, cfg.n_local_experts)
+    assert m["logits"][1] == T * E * 4
+    for name in ("topk_idx", "topk_w", "pair_row", "row_token"):
+        assert m[name][1] == T * k * 4
+    assert m["counts"][1] == E * 4 and m["offsets"][1] == (E + 1) * 4
+    assert m["h"][1] == rows * f * 2 and m["o"][1] == rows * d * 4
+    bad = dbrx(flags=2)
+    with pytest.raises(moe.MoeError):
+        moe.moe_workspace_map(bad)
 
 
 def test_init_pointer_checks():

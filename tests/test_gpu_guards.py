@@ -3,7 +3,10 @@ weight arena, the workspace and the output (and the in-place stack input)
 sit inside larger allocations whose margins hold a byte pattern; after
 loads, routing and forwards on the decode GEMVs, the grouped GEMM, an
 expert-parallel share and the stack, every margin must be intact (no kernel
-writes outside the buffers it was given)."""
+writes outside the buffers it was given).  Inside the workspace, every
+sub-buffer (moe_workspace_map) is guarded too: after a forward, the bytes of
+each region past what the call may write there, and the padding between
+regions, still hold the pattern."""
 import numpy as np
 import pytest
 
@@ -104,5 +107,64 @@ def test_dbrx_shapes_stay_inside_their_buffers(torch_mod):
             torch.cuda.synchronize()
             assert y.intact(), T
         assert arena.intact() and ws.intact()
+    finally:
+        layer.close()
+
+
+def _may_write(name, T, k, E, d, f, rt, decode_route, n_wg=None):
+    """Byte ranges (relative to the region) that a forward of T tokens may
+    write in workspace region `name`, given its routing."""
+    rows = int(rt["offsets"][-1])
+    n_active = int((rt["counts"] > 0).sum())
+    if name == "route_partials":
+        # the small-T router writes T of 16 token slots of each workgroup's
+        # 16 x 16 fp64 block (32 KiB at most)
+        return [(b * 16 * 16 * 8, (b * 16 + T) * 16 * 8) for b in range(n_wg)] if decode_route else []
+    sizes = {"logits": T * E * 4, "topk_idx": T * k * 4, "topk_w": T * k * 4, "counts": E * 4,
+             "offsets": (E + 1) * 4, "pair_row": T * k * 4, "row_token": rows * 4,
+             "active": (1 + n_active) * 4, "n_tiles": 4, "h": rows * f * 2, "o": rows * d * 4}
+    if name == "tiles":
+        return None      # checked through n_tiles below
+    return [(0, sizes[name])]
+
+
+@pytest.mark.parametrize("T,e_begin,n_local", [(3, 0, 0), (16, 2, 4), (40, 0, 0), (300, 6, 2)])
+def test_workspace_regions_stay_inside_themselves(torch_mod, T, e_begin, n_local):
+    """max_tokens is twice T, so every region has room past what the call
+    uses: an overrun (H into its tail, O past its rows, a routing array past
+    T entries) shows as a changed byte."""
+    import paper_2506_23635_amd as moe
+    torch = torch_mod
+    wl = TINY.with_(T=T)
+    layer, arena, ws = _layer(torch, wl, 2 * T, e_begin=e_begin, n_local=n_local)
+    try:
+        load_workload_host(layer, wl)
+        x_t, _ = x_device(wl)
+        y = torch.empty((T, wl.d), dtype=torch.int16, device="cuda")
+        ws.inner.fill_(PATTERN)
+        torch.cuda.synchronize()
+        layer.forward(0, x_t, y)
+        torch.cuda.synchronize()
+        after = ws.inner.cpu().numpy()
+        rt = layer.routing_tensors(layer.route(0, x_t))   # same routing; re-written in place
+        torch.cuda.synchronize()
+        m = moe.moe_workspace_map(layer.cfg)
+        E, k, d, f = wl.E, wl.k, wl.d, wl.f
+        decode_route = T <= 16 and E <= 16 and T * k <= 64
+        n_wg = (d // 8 + 63) // 64
+        allowed = np.zeros(after.size, dtype=bool)
+        n_tiles = int(np.frombuffer(after[m["n_tiles"][0]:m["n_tiles"][0] + 4].tobytes(), np.int32)[0])
+        for name, (off, nb) in m.items():
+            if name == "tiles":
+                spans = [(0, n_tiles * 8)]
+            else:
+                spans = _may_write(name, T, k, E, d, f, rt, decode_route, n_wg)
+            for a, b in spans:
+                assert b <= nb, (name, b, nb)
+                allowed[off + a: off + b] = True
+        bad = np.nonzero((after != PATTERN) & ~allowed)[0]
+        where = [n for n, (o, nb) in m.items() if bad.size and o <= bad[0] < o + nb]
+        assert bad.size == 0, (int(bad[0]), where)
+        assert ws.intact() and arena.intact()
     finally:
         layer.close()

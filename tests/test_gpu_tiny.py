@@ -6,8 +6,8 @@ import pytest
 import moe_inputs as mi
 import oracle
 import paper_2506_23635_amd as moe
-from harness import (bf16_f64, check_layer_output, host_experts, load_workload_host,
-                     make_layer, rel_l2, to_np_u16, x_device)
+from harness import (bf16_f64, check_chain, check_layer_output, host_experts, load_workload_host,
+                     make_layer, read_intermediates, rel_l2, to_np_u16, x_device)
 
 pytestmark = pytest.mark.gpu
 
@@ -250,6 +250,21 @@ def test_binding_rejects_bad_weights_before_load(torch_mod, tiny_layer):
     assert np.array_equal(_forward(torch, tiny_layer, x_t), before)
 
 
+def _chain(torch, layer, wl, x, x_t, y, e_begin=0, n_local=0, y_f32=False):
+    """check_chain on every token of the layer's last forward (routing
+    re-read from an identical moe_route, which leaves H and O in place)."""
+    rt = layer.routing_tensors(layer.route(0, x_t))
+    lg = oracle.router_logits(x, wl.router(), wl.bias())
+    idx, w = oracle.route_from_logits(lg, wl.k)
+    assert np.array_equal(rt["idx"], idx)
+    G, U, D = host_experts(wl, range(wl.E))
+    y64, y16, hb = oracle.layer_with_routing_ex(x, idx, w, G, U, D, e_begin=e_begin,
+                                                n_local=n_local, want_hb=True)
+    H, O = read_intermediates(torch, layer, int(rt["offsets"][-1]))
+    return check_chain(x, rt, H, O, y, {"y64": y64, "y16": y16, "hb": hb, "w": w},
+                       lambda e: (G[e], U[e], D[e]), y_f32=y_f32)
+
+
 @pytest.mark.parametrize("T", [1, 5, 16])
 def test_forward_decode_path(torch_mod, tiny_layer, T):
     torch = torch_mod
@@ -258,6 +273,8 @@ def test_forward_decode_path(torch_mod, tiny_layer, T):
     y = _forward(torch, tiny_layer, x_t)
     ref = _oracle_full(wl, x)
     check_layer_output(y, ref["y64"])
+    st = _chain(torch, tiny_layer, wl, x, x_t, y)
+    assert st["rows"] == T * wl.k
 
 
 @pytest.mark.parametrize("T", [17, 100, 300, 512])
@@ -268,6 +285,89 @@ def test_forward_gemm_path(torch_mod, tiny_layer, T):
     y = _forward(torch, tiny_layer, x_t)
     ref = _oracle_full(wl, x)
     check_layer_output(y, ref["y64"])
+    st = _chain(torch, tiny_layer, wl, x, x_t, y)
+    assert st["rows"] == T * wl.k
+
+
+@pytest.mark.parametrize("T", [1, 16, 300])
+def test_partial_f32_shares(torch_mod, T):
+    """MOE_PARTIAL_F32: a share writes its unrounded fp32 partial (Sec. 4.3:
+    what the all-reduce adds).  Its bf16 rounding is the bf16 partial of the
+    same share bit for bit (same kernels, same order), it passes the
+    per-element chain with the fp32 bound, and the four fp32 partials sum to
+    the full layer within the sum of their bounds."""
+    torch = torch_mod
+    wl = TINY.with_(T=T)
+    x_t, x = x_device(wl)
+    full = _oracle_full(wl, x)
+    total = np.zeros_like(full["y64"])
+    bound = np.zeros_like(full["y64"])
+    for s in range(4):
+        ys = {}
+        for flags in (0, moe.MOE_PARTIAL_F32):
+            layer = make_layer(wl, max_tokens=max(T, 16), e_begin=2 * s, n_local=2, flags=flags)
+            load_workload_host(layer, wl)
+            if flags:
+                y = torch.full((T, wl.d), 1.5, dtype=torch.float32, device="cuda")
+                layer.forward(0, x_t, y)
+                torch.cuda.synchronize()
+                ys[flags] = y.cpu().numpy()
+                st = _chain(torch, layer, wl, x, x_t, ys[flags], e_begin=2 * s, n_local=2,
+                            y_f32=True)
+                total += ys[flags]
+                bound += st["y_bound"]
+            else:
+                ys[flags] = _forward(torch, layer, x_t)
+            layer.close()
+        assert np.array_equal(oracle.bf16_round(ys[moe.MOE_PARTIAL_F32].astype(np.float64)), ys[0])
+    assert np.all(np.abs(total - full["y64"]) <= bound + 1e-12 * np.abs(full["y64"]))
+
+
+def test_routing_validity_rules(torch_mod):
+    """moe_forward accepts a routing only while it is the current result of
+    the last moe_route for that layer, T and x: an internal re-route, a stack
+    forward, another x or a reload of that layer's router make it stale
+    (MOE_E_STATE, nothing launched); routing from given logits accepts any x."""
+    torch = torch_mod
+    wl = TINY.with_(T=8, n_layers=2)
+    layer = make_layer(wl, max_tokens=16, n_layers=2)
+    try:
+        for li in range(2):
+            load_workload_host(layer, wl, layer_idx=li)
+        x_t, x = x_device(wl)
+        x2_t = x_t.flip(0).contiguous()
+        y = torch.zeros((8, wl.d), dtype=torch.int16, device="cuda")
+
+        def stale(r, xx=x_t, layer_idx=0):
+            y.fill_(7)
+            with pytest.raises(moe.MoeError) as ei:
+                layer.forward(layer_idx, xx, y, routing=r)
+            assert ei.value.status == -5
+            torch.cuda.synchronize()
+            assert bool((y == 7).all())
+
+        r = layer.route(0, x_t)
+        layer.forward(0, x_t, y, routing=r)          # current: accepted
+        stale(r, xx=x2_t)                             # computed from another x
+        stale(r, layer_idx=1)                         # another layer
+        layer.forward(0, x_t, y)                      # internal re-route
+        stale(r)
+        r = layer.route(0, x_t)
+        layer.forward_stack(x2_t.clone())             # the stack re-routes every layer
+        stale(r)
+        r = layer.route(0, x_t)
+        wr = torch.from_numpy(wl.router(0)).cuda()
+        layer.load_router(0, wr)                      # same values, still a reload
+        stale(r)
+        r = layer.route(1, x_t)
+        layer.load_router(0, wr)                      # another layer's reload: still valid
+        layer.forward(1, x_t, y, routing=r)
+        lg = oracle.router_logits(x, wl.router(0))
+        r = layer.route(0, None, T=8, logits_in=torch.from_numpy(lg).cuda())
+        layer.forward(0, x2_t, y, routing=r)          # given logits: any x
+        torch.cuda.synchronize()
+    finally:
+        layer.close()
 
 
 @pytest.mark.parametrize("T", [3, 200])

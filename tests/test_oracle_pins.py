@@ -336,6 +336,50 @@ def test_layer_single_expert_is_plain_swiglu_ffn():
     assert np.array_equal(r["y"], oracle.bf16_round(r["y64"]))
 
 
+def test_layer_exact_form_single_expert_is_unrounded_swiglu():
+    """The information-only exact form (no H rounding) of E = 1, k = 1 is the
+    textbook SwiGLU FFN in fp64 (library matmul, scipy's logistic) to
+    rounding; the per-pair H it returns is the rounded form's hb."""
+    T, d, f = 5, 48, 80
+    x = mi.gen_bf16(6, mi.stream_id(mi.KIND_X), (T, d), 1.0)
+    g_w, u_w, d_w = _rand_expert(6, d, f, sigma=0.1)
+    idx = np.zeros((T, 1), np.int32)
+    w = np.ones((T, 1))
+    y64, y16, hb = oracle.layer_with_routing_ex(x, idx, w, [g_w], [u_w], [d_w], round_h=False,
+                                                want_hb=True)
+    g = _f64(x) @ _f64(g_w)
+    u = _f64(x) @ _f64(u_w)
+    ref = (g * scipy.special.expit(g) * u) @ _f64(d_w)
+    assert np.allclose(y64, ref, rtol=1e-12, atol=1e-12)
+    assert np.array_equal(y16, oracle.bf16_round(y64))
+    hb1, _ = oracle.expert_glu(x, g_w, u_w, d_w)
+    assert np.array_equal(hb[:, 0, :], hb1)
+
+
+def test_layer_with_routing_ex_rounded_form_is_the_layer():
+    """With H rounded, the extended entry point gives the layer's bits, and
+    each local pair's H row is that expert's hb for the token (rows of
+    non-local pairs stay zero)."""
+    x, wr, G, U, D = _tiny_inputs(T=9)
+    r = oracle.layer(x, wr, None, G, U, D, k=2, e_begin=2, n_local=4)
+    y64, y16, hb = oracle.layer_with_routing_ex(x, r["idx"], r["w"], G, U, D, e_begin=2,
+                                                n_local=4, want_hb=True)
+    assert np.array_equal(y64, r["y64"]) and np.array_equal(y16, r["y"])
+    for t in range(9):
+        for j in range(2):
+            e = r["idx"][t, j]
+            if 2 <= e < 6:
+                h1, _ = oracle.expert_glu(x[t:t + 1], G[e], U[e], D[e])
+                assert np.array_equal(hb[t, j], h1[0])
+            else:
+                assert np.all(hb[t, j] == 0)
+    # the exact form differs from the rounded one by about the bf16 step of H
+    e64, _, _ = oracle.layer_with_routing_ex(x, r["idx"], r["w"], G, U, D, e_begin=2, n_local=4,
+                                             round_h=False)
+    rel = np.linalg.norm(y64 - e64) / np.linalg.norm(e64)
+    assert 1e-5 < rel < 4e-3
+
+
 def test_layer_zero_input_gives_zero():
     x, wr, G, U, D = _tiny_inputs()
     x[:] = 0
