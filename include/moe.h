@@ -189,6 +189,27 @@ MOE_API moe_status moe_forward(moe_ctx *ctx, int32_t layer, const uint16_t *x,
                        int32_t T, const moe_routing *r, void *y,
                        moe_stream_t stream);
 
+/* For callers that cannot allocate device memory when they call (code under
+ * HIP graph capture, tight serving loops, harnesses that forbid allocation).
+ * Same as moe_forward(ctx, layer, x, T, NULL, y, stream) -- routing, experts
+ * and combine; y bf16 [T, d], or fp32 with MOE_PARTIAL_F32 -- but the
+ * routing arrays and the intermediates H and O live in a static device array
+ * of MOE_STATIC_SCRATCH_BYTES that the library holds on each GPU it runs on
+ * until the process ends, not in the context's workspace.  The call leaves
+ * the workspace untouched (a routing from moe_route stays valid) and calls no
+ * allocating routine.  T is limited by max_tokens and by the scratch: the
+ * workspace that moe_workspace_bytes reports for max_tokens = T must fit in
+ * MOE_STATIC_SCRATCH_BYTES (T <= 40 at d 6144, f 10752, 16 experts, top-4);
+ * beyond either, MOE_E_CAPACITY and nothing is enqueued.  The context's
+ * device must be current.  Every call on a GPU shares that GPU's array and
+ * leaves its contents behind: calls that overlap on one GPU (two streams, two
+ * host threads) race and must be ordered by the caller.  The first call on a
+ * device looks up the array's device address (a runtime query, no
+ * allocation); its failure returns MOE_E_HIP. */
+#define MOE_STATIC_SCRATCH_BYTES (8u << 20)
+MOE_API moe_status moe_forward_static(moe_ctx *ctx, int32_t layer, const uint16_t *x,
+                                      int32_t T, void *y, moe_stream_t stream);
+
 /* Sec. 4.1 (all layers' experts resident in one prestacked array, indexed
  * per layer) and Sec. 2.1 (one MoE FFN per decoder layer).  All n_layers
  * layers in order on T tokens, in place: for each layer l,

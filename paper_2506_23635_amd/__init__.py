@@ -25,7 +25,8 @@ STATUS_NAMES = {0: "MOE_OK", -1: "MOE_E_ARG", -2: "MOE_E_SHAPE", -3: "MOE_E_ALIG
 
 EXPORTED = ["moe_weight_bytes", "moe_workspace_bytes", "moe_workspace_map", "moe_init",
             "moe_load_expert",
-            "moe_load_router", "moe_route", "moe_forward", "moe_forward_stack",
+            "moe_load_router", "moe_route", "moe_forward", "moe_forward_static",
+            "moe_forward_stack",
             "moe_intermediates", "moe_profile_enable", "moe_profile_read", "moe_destroy",
             "moe_last_error", "moe_status_string", "moe_diag_stream_read"]
 
@@ -81,6 +82,7 @@ def lib():
         L.moe_load_router.argtypes = [P, I, P, P, I, P]
         L.moe_route.argtypes = [P, I, P, I, P, ctypes.POINTER(MoeRouting), P]
         L.moe_forward.argtypes = [P, I, P, I, ctypes.POINTER(MoeRouting), P, P]
+        L.moe_forward_static.argtypes = [P, I, P, I, P, P]
         L.moe_forward_stack.argtypes = [P, P, I, P]
         L.moe_intermediates.argtypes = [P, ctypes.POINTER(P), ctypes.POINTER(P)]
         L.moe_profile_enable.argtypes = [P, I]
@@ -93,7 +95,7 @@ def lib():
         L.moe_status_string.restype = ctypes.c_char_p
         L.moe_diag_stream_read.argtypes = [P, ctypes.c_uint64, P, P]
         for fn in ("moe_init", "moe_load_expert", "moe_load_router", "moe_route", "moe_forward",
-                   "moe_forward_stack", "moe_intermediates", "moe_profile_enable",
+                   "moe_forward_static", "moe_forward_stack", "moe_intermediates", "moe_profile_enable",
                    "moe_profile_read", "moe_diag_stream_read"):
             getattr(L, fn).restype = ctypes.c_int
         _lib = L
@@ -155,6 +157,10 @@ def moe_route(ctx, layer, x_ptr, T, logits_in_ptr=None, stream=0) -> MoeRouting:
 def moe_forward(ctx, layer, x_ptr, T, routing, y_ptr, stream=0):
     rp = ctypes.byref(routing) if routing is not None else None
     _check(ctx, lib().moe_forward(ctx, layer, x_ptr, T, rp, y_ptr, stream))
+
+
+def moe_forward_static(ctx, layer, x_ptr, T, y_ptr, stream=0):
+    _check(ctx, lib().moe_forward_static(ctx, layer, x_ptr, T, y_ptr, stream))
 
 
 def moe_forward_stack(ctx, x_ptr, T, stream=0):
@@ -315,6 +321,15 @@ class MoeLayer:
         ytypes = (self.torch.float32,) if self.cfg.flags & MOE_PARTIAL_F32 else bf
         moe_forward(self.ctx, layer, _tensor_ptr(x, "x", n, bf, self.device), T, routing,
                     _tensor_ptr(y, "y", n, ytypes, self.device), self.stream)
+
+    def forward_static(self, layer, x, y, T=None):
+        """moe_forward_static: the layer with internal routing on the
+        library's static device scratch (no workspace use, no allocation)."""
+        T = self._tokens(x, T)
+        n, bf = T * self.cfg.d_model, _bf16_types(self.torch)
+        ytypes = (self.torch.float32,) if self.cfg.flags & MOE_PARTIAL_F32 else bf
+        moe_forward_static(self.ctx, layer, _tensor_ptr(x, "x", n, bf, self.device), T,
+                           _tensor_ptr(y, "y", n, ytypes, self.device), self.stream)
 
     def forward_stack(self, x, T=None):
         T = self._tokens(x, T)

@@ -10,6 +10,7 @@
 #include <cstdio>
 #include <cstdlib>
 #include <cstring>
+#include <mutex>
 #include <new>
 #include <string>
 #include <algorithm>
@@ -101,17 +102,44 @@ Layout make_layout(const moe_config* c)
 
 thread_local std::string g_init_error;
 
+// Device views of one workspace: the context's own, or the library's static
+// scratch (moe_forward_static).
+struct WsView {
+    uint8_t* base;
+    size_t dpart_off, h_off, o_off;
+    moe::RouteView rv;
+};
+
+WsView make_ws_view(uint8_t* w, const Layout& L)
+{
+    WsView v{};
+    v.base = w;
+    v.dpart_off = L.dpart_off;
+    v.h_off = L.h_off;
+    v.o_off = L.o_off;
+    v.rv.logits = reinterpret_cast<float*>(w + L.logits_off);
+    v.rv.topk_idx = reinterpret_cast<int32_t*>(w + L.idx_off);
+    v.rv.topk_w = reinterpret_cast<float*>(w + L.w_off);
+    v.rv.counts = reinterpret_cast<int32_t*>(w + L.counts_off);
+    v.rv.offsets = reinterpret_cast<int32_t*>(w + L.offsets_off);
+    v.rv.pair_row = reinterpret_cast<int32_t*>(w + L.pair_row_off);
+    v.rv.row_token = reinterpret_cast<int32_t*>(w + L.row_token_off);
+    v.rv.active = reinterpret_cast<int32_t*>(w + L.active_off);
+    v.rv.tiles = reinterpret_cast<int32_t*>(w + L.tiles_off);
+    v.rv.n_tiles = reinterpret_cast<int32_t*>(w + L.n_tiles_off);
+    return v;
+}
+
 }  // namespace
 
 struct moe_ctx {
     moe_config cfg;
     Layout L;
     uint8_t* arena;
-    uint8_t* ws;
+    WsView ws;                            // the caller's workspace
     std::vector<uint8_t> router_loaded;   // [n_layers]
     std::vector<uint8_t> has_bias;        // [n_layers]
     std::vector<uint8_t> expert_loaded;   // [n_layers * n_local]
-    moe::RouteView rv;
     // per-kernel timing (moe_profile_*): an event pair around each launch
     bool prof_on;
     std::vector<hipEvent_t> prof_events;   // 2 per launch slot
@@ -173,8 +201,8 @@ moe_status check_layer(moe_ctx* ctx, int layer)
     return MOE_OK;
 }
 
-moe_status do_route(moe_ctx* ctx, int layer, const uint16_t* x, int T, const float* logits_in,
-                    hipStream_t s)
+moe_status do_route(moe_ctx* ctx, const WsView& ws, int layer, const uint16_t* x, int T,
+                    const float* logits_in, hipStream_t s)
 {
     const moe_config& c = ctx->cfg;
     uint8_t* lb = layer_base(ctx, layer);
@@ -184,24 +212,24 @@ moe_status do_route(moe_ctx* ctx, int layer, const uint16_t* x, int T, const flo
     const int tile_rows = moe_prefill_tile_rows();
     hipError_t e;
     if (!logits_in && moe_route_decode_ok(T, c.n_experts, c.top_k)) {
-        double* dpart = reinterpret_cast<double*>(ctx->ws + ctx->L.dpart_off);
+        double* dpart = reinterpret_cast<double*>(ws.base + ws.dpart_off);
         e = timed(ctx, MOE_K_ROUTE, s, [&] {
             return moe_launch_route_decode(x, wrT, bias, dpart, T, c.d_model, c.n_experts,
                                            c.top_k, c.expert_begin, c.n_local_experts, tile_rows,
-                                           &ctx->rv, s);
+                                           &ws.rv, s);
         });
         if (e != hipSuccess) return hip_fail(ctx, e, "route kernel launch");
     } else {
         if (!logits_in) {
             e = timed(ctx, MOE_K_ROUTER, s, [&] {
                 return moe_launch_router_select(x, wrT, bias, T, c.d_model, c.n_experts,
-                                                c.top_k, &ctx->rv, s);
+                                                c.top_k, &ws.rv, s);
             });
             if (e != hipSuccess) return hip_fail(ctx, e, "router kernel launch");
         }
         e = timed(ctx, MOE_K_ROUTE, s, [&] {
             return moe_launch_route(logits_in, T, c.n_experts, c.top_k, c.expert_begin,
-                                    c.n_local_experts, tile_rows, &ctx->rv, s);
+                                    c.n_local_experts, tile_rows, &ws.rv, s);
         });
         if (e != hipSuccess) return hip_fail(ctx, e, "route kernel launch");
     }
@@ -210,23 +238,25 @@ moe_status do_route(moe_ctx* ctx, int layer, const uint16_t* x, int T, const flo
 
 void fill_routing(moe_ctx* ctx, int layer, int T, moe_routing* out)
 {
-    out->logits = ctx->rv.logits;
-    out->topk_idx = ctx->rv.topk_idx;
-    out->topk_w = ctx->rv.topk_w;
-    out->counts = ctx->rv.counts;
-    out->offsets = ctx->rv.offsets;
-    out->pair_row = ctx->rv.pair_row;
-    out->row_token = ctx->rv.row_token;
+    const moe::RouteView& rv = ctx->ws.rv;
+    out->logits = rv.logits;
+    out->topk_idx = rv.topk_idx;
+    out->topk_w = rv.topk_w;
+    out->counts = rv.counts;
+    out->offsets = rv.offsets;
+    out->pair_row = rv.pair_row;
+    out->row_token = rv.row_token;
     out->T = T;
     out->layer = layer;
 }
 
-moe_status run_experts(moe_ctx* ctx, int layer, const uint16_t* x, int T, hipStream_t s)
+moe_status run_experts(moe_ctx* ctx, const WsView& ws, int layer, const uint16_t* x, int T,
+                       hipStream_t s)
 {
     const moe_config& c = ctx->cfg;
     const uint8_t* experts = layer_base(ctx, layer) + ctx->L.experts_off;
-    uint16_t* H = reinterpret_cast<uint16_t*>(ctx->ws + ctx->L.h_off);
-    float* O = reinterpret_cast<float*>(ctx->ws + ctx->L.o_off);
+    uint16_t* H = reinterpret_cast<uint16_t*>(ws.base + ws.h_off);
+    float* O = reinterpret_cast<float*>(ws.base + ws.o_off);
     hipError_t e;
     if (T <= kDecodeMaxTokens) {
         moe::DecodeArgs a;
@@ -236,10 +266,10 @@ moe_status run_experts(moe_ctx* ctx, int layer, const uint16_t* x, int T, hipStr
         a.x = x;
         a.H = H;
         a.O = O;
-        a.active = ctx->rv.active;
-        a.counts = ctx->rv.counts;
-        a.offsets = ctx->rv.offsets;
-        a.row_token = ctx->rv.row_token;
+        a.active = ws.rv.active;
+        a.counts = ws.rv.counts;
+        a.offsets = ws.rv.offsets;
+        a.row_token = ws.rv.row_token;
         a.d = c.d_model;
         a.f = c.ffn_dim;
         a.e_begin = c.expert_begin;
@@ -256,10 +286,10 @@ moe_status run_experts(moe_ctx* ctx, int layer, const uint16_t* x, int T, hipStr
         a.x = x;
         a.H = H;
         a.O = O;
-        a.offsets = ctx->rv.offsets;
-        a.row_token = ctx->rv.row_token;
-        a.tiles = ctx->rv.tiles;
-        a.n_tiles = ctx->rv.n_tiles;
+        a.offsets = ws.rv.offsets;
+        a.row_token = ws.rv.row_token;
+        a.tiles = ws.rv.tiles;
+        a.n_tiles = ws.rv.n_tiles;
         a.d = c.d_model;
         a.f = c.ffn_dim;
         a.e_begin = c.expert_begin;
@@ -272,6 +302,20 @@ moe_status run_experts(moe_ctx* ctx, int layer, const uint16_t* x, int T, hipStr
         e = timed(ctx, MOE_K_GEMM_DOWN, s, [&] { return moe_launch_gemm_down(&a, s); });
         if (e != hipSuccess) return hip_fail(ctx, e, "grouped GEMM down kernel launch");
     }
+    return MOE_OK;
+}
+
+// The weighted combine of the routed rows of ws: into y (bf16), y32 (fp32)
+// or, with x_residual, in place x = bf16(x + y).
+moe_status combine(moe_ctx* ctx, const WsView& ws, int T, uint16_t* y, float* y32,
+                   uint16_t* x_residual, hipStream_t s)
+{
+    hipError_t e = timed(ctx, MOE_K_COMBINE, s, [&] {
+        return moe_launch_combine(reinterpret_cast<const float*>(ws.base + ws.o_off),
+                                  ws.rv.pair_row, ws.rv.topk_w, T, ctx->cfg.d_model,
+                                  ctx->cfg.top_k, y, y32, x_residual, s);
+    });
+    if (e != hipSuccess) return hip_fail(ctx, e, "combine kernel launch");
     return MOE_OK;
 }
 
@@ -288,6 +332,36 @@ void pack_host(const uint16_t* src, int K, int N, uint8_t* dst, int rt_mul, int 
             for (int i = 0; i < 8; ++i) p[i] = src[(size_t)(k0 + i) * N + n];
         }
     }
+}
+
+// The static scratch of moe_forward_static: one array per GPU, held until
+// the process ends.  Host code never uses the array's name as an address
+// (on the host it is only a stand-in for the device symbol); the device
+// address is looked up once per device and kept in g_scratch_ptr.
+static __device__ __align__(256) uint8_t scratch[MOE_STATIC_SCRATCH_BYTES];
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kMaxDevices];
+
+// The current device's address of `scratch`, looked up on the first call
+// on that device (with the device current), then reused.
+moe_status scratch_ptr(moe_ctx* ctx, uint8_t** out)
+{
+    int dev = 0;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return hip_fail(ctx, e, "hipGetDevice");
+    if (dev < 0 || dev >= kMaxDevices) return fail(ctx, MOE_E_HIP, "device index past the scratch table");
+    std::lock_guard<std::mutex> lock(g_scratch_mu);
+    if (!g_scratch_ptr[dev]) {
+        void* p = nullptr;
+        e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+        if (e != hipSuccess) return hip_fail(ctx, e, "hipGetSymbolAddress of the static scratch");
+        if (!p) return fail(ctx, MOE_E_HIP, "hipGetSymbolAddress returned NULL for the static scratch");
+        g_scratch_ptr[dev] = p;
+    }
+    *out = static_cast<uint8_t*>(g_scratch_ptr[dev]);
+    return MOE_OK;
 }
 
 }  // namespace
@@ -330,21 +404,10 @@ moe_status moe_init(const moe_config* cfg, void* weight_arena, void* workspace, 
     c->cfg = *cfg;
     c->L = make_layout(cfg);
     c->arena = static_cast<uint8_t*>(weight_arena);
-    c->ws = static_cast<uint8_t*>(workspace);
+    c->ws = make_ws_view(static_cast<uint8_t*>(workspace), c->L);
     c->router_loaded.assign(cfg->n_layers, 0);
     c->has_bias.assign(cfg->n_layers, 0);
     c->expert_loaded.assign((size_t)cfg->n_layers * cfg->n_local_experts, 0);
-    uint8_t* w = c->ws;
-    c->rv.logits = reinterpret_cast<float*>(w + c->L.logits_off);
-    c->rv.topk_idx = reinterpret_cast<int32_t*>(w + c->L.idx_off);
-    c->rv.topk_w = reinterpret_cast<float*>(w + c->L.w_off);
-    c->rv.counts = reinterpret_cast<int32_t*>(w + c->L.counts_off);
-    c->rv.offsets = reinterpret_cast<int32_t*>(w + c->L.offsets_off);
-    c->rv.pair_row = reinterpret_cast<int32_t*>(w + c->L.pair_row_off);
-    c->rv.row_token = reinterpret_cast<int32_t*>(w + c->L.row_token_off);
-    c->rv.active = reinterpret_cast<int32_t*>(w + c->L.active_off);
-    c->rv.tiles = reinterpret_cast<int32_t*>(w + c->L.tiles_off);
-    c->rv.n_tiles = reinterpret_cast<int32_t*>(w + c->L.n_tiles_off);
     c->route_valid = false;
     c->route_layer = -1;
     c->route_T = 0;
@@ -458,7 +521,7 @@ moe_status moe_route(moe_ctx* ctx, int32_t layer, const uint16_t* x, int32_t T,
     } else if (misaligned(logits_in)) {
         return fail(ctx, MOE_E_ALIGN, "logits_in must be 16-byte aligned");
     }
-    moe_status st = do_route(ctx, layer, x, T, logits_in, static_cast<hipStream_t>(stream));
+    moe_status st = do_route(ctx, ctx->ws, layer, x, T, logits_in, static_cast<hipStream_t>(stream));
     if (st != MOE_OK) return st;
     ctx->route_valid = true;
     ctx->route_layer = layer;
@@ -481,7 +544,7 @@ moe_status moe_forward(moe_ctx* ctx, int32_t layer, const uint16_t* x, int32_t T
     if (misaligned(x) || misaligned(y)) return fail(ctx, MOE_E_ALIGN, "x and y must be 16-byte aligned");
     hipStream_t s = static_cast<hipStream_t>(stream);
     if (r) {
-        if (!ctx->route_valid || r->T != T || r->layer != layer || r->logits != ctx->rv.logits ||
+        if (!ctx->route_valid || r->T != T || r->layer != layer || r->logits != ctx->ws.rv.logits ||
             ctx->route_T != T || ctx->route_layer != layer)
             return fail(ctx, MOE_E_STATE,
                         "routing is not the current result of the last moe_route for this layer and T");
@@ -489,20 +552,14 @@ moe_status moe_forward(moe_ctx* ctx, int32_t layer, const uint16_t* x, int32_t T
             return fail(ctx, MOE_E_STATE, "routing was computed from a different x");
     } else {
         ctx->route_valid = false;   // the views are about to be overwritten
-        st = do_route(ctx, layer, x, T, nullptr, s);
+        st = do_route(ctx, ctx->ws, layer, x, T, nullptr, s);
         if (st != MOE_OK) return st;
     }
-    st = run_experts(ctx, layer, x, T, s);
+    st = run_experts(ctx, ctx->ws, layer, x, T, s);
     if (st != MOE_OK) return st;
     const bool f32_out = (ctx->cfg.flags & MOE_PARTIAL_F32) != 0;
-    hipError_t e = timed(ctx, MOE_K_COMBINE, s, [&] {
-        return moe_launch_combine(reinterpret_cast<const float*>(ctx->ws + ctx->L.o_off),
-                                  ctx->rv.pair_row, ctx->rv.topk_w, T, ctx->cfg.d_model,
-                                  ctx->cfg.top_k, f32_out ? nullptr : static_cast<uint16_t*>(y),
-                                  f32_out ? static_cast<float*>(y) : nullptr, nullptr, s);
-    });
-    if (e != hipSuccess) return hip_fail(ctx, e, "combine kernel launch");
-    return MOE_OK;
+    return combine(ctx, ctx->ws, T, f32_out ? nullptr : static_cast<uint16_t*>(y),
+                   f32_out ? static_cast<float*>(y) : nullptr, nullptr, s);
 }
 
 moe_status moe_forward_stack(moe_ctx* ctx, uint16_t* x_inout, int32_t T, moe_stream_t stream)
@@ -520,25 +577,54 @@ moe_status moe_forward_stack(moe_ctx* ctx, uint16_t* x_inout, int32_t T, moe_str
     hipStream_t s = static_cast<hipStream_t>(stream);
     ctx->route_valid = false;   // the routing views are overwritten layer by layer
     for (int l = 0; l < ctx->cfg.n_layers; ++l) {
-        moe_status st = do_route(ctx, l, x_inout, T, nullptr, s);
+        moe_status st = do_route(ctx, ctx->ws, l, x_inout, T, nullptr, s);
         if (st != MOE_OK) return st;
-        st = run_experts(ctx, l, x_inout, T, s);
+        st = run_experts(ctx, ctx->ws, l, x_inout, T, s);
         if (st != MOE_OK) return st;
-        hipError_t e = timed(ctx, MOE_K_COMBINE, s, [&] {
-            return moe_launch_combine(reinterpret_cast<const float*>(ctx->ws + ctx->L.o_off),
-                                      ctx->rv.pair_row, ctx->rv.topk_w, T, ctx->cfg.d_model,
-                                      ctx->cfg.top_k, nullptr, nullptr, x_inout, s);
-        });
-        if (e != hipSuccess) return hip_fail(ctx, e, "combine kernel launch");
+        st = combine(ctx, ctx->ws, T, nullptr, nullptr, x_inout, s);
+        if (st != MOE_OK) return st;
     }
     return MOE_OK;
+}
+
+moe_status moe_forward_static(moe_ctx* ctx, int32_t layer, const uint16_t* x, int32_t T, void* y,
+                              moe_stream_t stream)
+{
+    if (!ctx) return MOE_E_ARG;
+    if (T < 0) return fail(ctx, MOE_E_ARG, "T is negative");
+    if (T > ctx->cfg.max_tokens) return fail(ctx, MOE_E_CAPACITY, "T exceeds max_tokens");
+    moe_status st = check_layer(ctx, layer);
+    if (st != MOE_OK) return st;
+    if (T == 0) return MOE_OK;
+    if (!x || !y) return fail(ctx, MOE_E_ARG, "x or y is NULL");
+    if (misaligned(x) || misaligned(y)) return fail(ctx, MOE_E_ALIGN, "x and y must be 16-byte aligned");
+    // the workspace layout of this T, carved from the static scratch
+    moe_config c = ctx->cfg;
+    c.max_tokens = T;
+    const Layout L = make_layout(&c);
+    if (L.ws_bytes > MOE_STATIC_SCRATCH_BYTES)
+        return fail(ctx, MOE_E_CAPACITY,
+                    "T needs " + std::to_string(L.ws_bytes) + " bytes of scratch; the static scratch holds " +
+                        std::to_string((size_t)MOE_STATIC_SCRATCH_BYTES));
+    uint8_t* base = nullptr;
+    st = scratch_ptr(ctx, &base);
+    if (st != MOE_OK) return st;
+    const WsView ws = make_ws_view(base, L);
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    st = do_route(ctx, ws, layer, x, T, nullptr, s);
+    if (st != MOE_OK) return st;
+    st = run_experts(ctx, ws, layer, x, T, s);
+    if (st != MOE_OK) return st;
+    const bool f32_out = (ctx->cfg.flags & MOE_PARTIAL_F32) != 0;
+    return combine(ctx, ws, T, f32_out ? nullptr : static_cast<uint16_t*>(y),
+                   f32_out ? static_cast<float*>(y) : nullptr, nullptr, s);
 }
 
 moe_status moe_intermediates(const moe_ctx* ctx, const uint16_t** h, const float** o)
 {
     if (!ctx) return MOE_E_ARG;
-    if (h) *h = reinterpret_cast<const uint16_t*>(ctx->ws + ctx->L.h_off);
-    if (o) *o = reinterpret_cast<const float*>(ctx->ws + ctx->L.o_off);
+    if (h) *h = reinterpret_cast<const uint16_t*>(ctx->ws.base + ctx->ws.h_off);
+    if (o) *o = reinterpret_cast<const float*>(ctx->ws.base + ctx->ws.o_off);
     return MOE_OK;
 }
 
