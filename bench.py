@@ -385,6 +385,78 @@ def stack_section(steps, warmup):
     return out
 
 
+def gemm_timeline(layer, x):
+    """One forward with the per-workgroup GEMM timeline on
+    (moe_profile_gemm_timeline), its two GEMMs also event-timed: for each
+    grouped GEMM, the clock its tiles ran at (shader-clock cycles over the
+    constant wall-clock counter, whose rate the runtime reports, so no
+    profiler offset enters), the span, how busy the CUs were, the mean tile
+    time per number of 64-row pairs, the gap between consecutive tiles on a
+    CU, and the MFMA fraction against the spec peak and against the peak at
+    the measured clock."""
+    import numpy as np
+    import torch
+    import paper_2506_23635_amd as moe
+    n = 8192
+    bufs = [torch.zeros(n * 8, dtype=torch.int64, device="cuda") for _ in range(2)]
+    y = torch.empty((x.shape[0], layer.cfg.d_model), dtype=torch.int16, device="cuda")
+    layer.forward(0, x, y)
+    torch.cuda.synchronize()
+    moe.moe_profile_gemm_timeline(layer.ctx, bufs[0].data_ptr(), bufs[1].data_ptr(), n)
+    moe.moe_profile_enable(layer.ctx, 16)
+    layer.forward(0, x, y)
+    torch.cuda.synchronize()
+    prof, _ = moe.moe_profile_read(layer.ctx)
+    moe.moe_profile_enable(layer.ctx, 0)
+    moe.moe_profile_gemm_timeline(layer.ctx, None, None, 0)
+    d, f = layer.cfg.d_model, layer.cfg.ffn_dim
+    # the counter's rate from this launch: its ticks over the same GEMM's
+    # event time (the runtime's wall-clock attribute does not describe this
+    # counter on this part: it reports 30 MHz, the ticks run at 100 MHz)
+    t0 = bufs[0].cpu().numpy().view(np.uint64).reshape(n, 8)
+    t0 = t0[t0[:, 1] > 0]
+    ev0 = prof["gemm_gateup"][0] / max(prof["gemm_gateup"][1], 1) * 1e-3
+    hz = float(t0[:, 1].max() - t0[:, 0].min()) / ev0
+    out = {"counter_mhz": hz / 1e6}
+    for name, buf, K in (("gemm_gateup", bufs[0], d), ("gemm_down", bufs[1], f)):
+        t = buf.cpu().numpy().view(np.uint64).reshape(n, 8)
+        t = t[t[:, 1] > 0]
+        r0, r1 = t[:, 0].astype(np.int64), t[:, 1].astype(np.int64)
+        c0, c1 = t[:, 2].astype(np.int64), t[:, 3].astype(np.int64)
+        hw, xcc = t[:, 4] & 0xFFFFFFFF, t[:, 4] >> 32
+        rows = ((t[:, 5] >> 32) & 0xFFFF).astype(np.int64)
+        cu = (xcc << 8) | ((hw >> 8) & 0xFF)
+        tick_us = 1e6 / hz
+        dur_us = (r1 - r0) * tick_us
+        span_us = (r1.max() - r0.min()) * tick_us
+        n_cu = len(np.unique(cu))
+        clock = (c1 - c0).sum() / ((r1 - r0).sum() / hz) / 1e9
+        per_wg_clock = (c1 - c0) / ((r1 - r0) / hz) / 1e9
+        gaps = []
+        for u in np.unique(cu):
+            sel = np.nonzero(cu == u)[0]
+            order = sel[np.argsort(r0[sel])]
+            gaps.extend(((r0[order[1:]] - r1[order[:-1]]) * tick_us).tolist())
+        pairs = (rows + 63) // 64
+        flops = float(rows.sum()) * 256 * K * 2        # each workgroup: rows x 256 features x K
+        ev_ms = prof[name][0] / max(prof[name][1], 1)
+        tf = flops / (ev_ms * 1e-3) / 1e12
+        out[name] = {
+            "workgroups": int(len(t)), "cus": int(n_cu), "span_us": float(span_us),
+            "event_us": ev_ms * 1e3,
+            "clock_ghz": float(clock), "clock_ghz_p5_p95": [float(np.percentile(per_wg_clock, 5)),
+                                                            float(np.percentile(per_wg_clock, 95))],
+            "cu_busy_frac": float(dur_us.sum() / (n_cu * span_us)),
+            "tile_us_by_pairs": {int(p): float(dur_us[pairs == p].mean()) for p in np.unique(pairs)},
+            "tiles_by_pairs": {int(p): int((pairs == p).sum()) for p in np.unique(pairs)},
+            "gap_us_mean": float(np.mean(gaps)) if gaps else 0.0,
+            "tflops": tf, "mfma_frac": tf / MFMA_BF16_PEAK_TFLOPS,
+            "mfma_frac_at_clock": tf / (MFMA_BF16_PEAK_TFLOPS * clock / 2.4),
+        }
+    del bufs
+    return out
+
+
 def stream_read_gbs(nbytes=4 << 30, reps=20):
     """GB/s of the library's plain streaming read (moe_diag_stream_read) over
     a 4 GiB buffer, far past the 256 MB last-level cache: the achievable HBM
@@ -569,6 +641,8 @@ def main():
     ap.add_argument("--stack-steps", type=int, default=20)
     ap.add_argument("--prefill-only", action="store_true",
                     help="time only the prefill layer (for counter collection)")
+    ap.add_argument("--timeline", action="store_true",
+                    help="with --prefill-only: also record the per-workgroup GEMM timeline")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="also run one 1 GiB device copy of known size (counter calibration)")
     ap.add_argument("--cpu-oracle-all", action="store_true",
@@ -617,8 +691,15 @@ def main():
         player, px = setup_layer(pw, max_tokens=pw.T)
         pms, pkern, prt, _ = time_layer(player, px, args.prefill_steps, 2)
         rows = int(prt["offsets"][-1])
+        tl = None
+        if args.timeline:
+            # after a pause, then back to back: the clock the power
+            # controller grants moves from one GEMM to the next
+            time.sleep(1.0)
+            tl = [gemm_timeline(player, px) for _ in range(5)]
         print(json.dumps({"prefill_ms": pms, "tflops": 2.0 * rows * 3 * pw.d * pw.f / (pms * 1e-3) / 1e12,
-                          "kernels_ms": {k: v["ms_per_launch"] for k, v in pkern.items()}}),
+                          "kernels_ms": {k: v["ms_per_launch"] for k, v in pkern.items()},
+                          "timeline": tl}),
               flush=True)
         player.close()
         del player, px
@@ -669,7 +750,10 @@ def main():
         tflops = flops / (pms * 1e-3) / 1e12
         g1 = pkern["gemm_gateup"]
         g1_flops = 2.0 * rows * 2 * pw.d * pw.f
+        log("prefill GEMM timeline ...")
+        tl = gemm_timeline(player, px)
         prefill = {
+            "timeline": tl,
             "workload": "dbrx_moe_layer_prefill", "T": pw.T, "tokens_per_s": pw.T / (pms * 1e-3),
             "ms_per_layer": pms, "tflops": tflops, "mfma_frac": tflops / MFMA_BF16_PEAK_TFLOPS,
             "expert_counts": prt["counts"].tolist(),

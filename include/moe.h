@@ -268,6 +268,19 @@ MOE_API moe_status moe_profile_enable(moe_ctx *ctx, int32_t max_launches);
 MOE_API moe_status moe_profile_read(moe_ctx *ctx, double *total_ms,
                                     int64_t *launches, int64_t *dropped);
 
+/* Measurement: a per-workgroup timeline of the grouped GEMMs (T > 16).
+ * With buffers set (device, uint64 [max_wg][8] each, zeroed by the caller;
+ * either may be NULL), every later forward on ctx that takes the GEMM path
+ * records, for each GEMM workgroup b < max_wg that has a tile: [0], [1] the
+ * constant 100 MHz counter at the tile's start and end, [2], [3] the shader
+ * clock counter at start and end (so [3]-[2] over ([1]-[0]) / 1e8 s is the
+ * clock the tile ran at), [4] HW_ID | XCC_ID << 32 of its CU, [5] feature
+ * tile | token tile << 16 | rows << 32 | expert << 48.  Workgroups without a
+ * tile leave their entry untouched.  max_wg == 0 turns it off.  The
+ * recording adds one barrier per workgroup. */
+MOE_API moe_status moe_profile_gemm_timeline(moe_ctx *ctx, uint64_t *gateup, uint64_t *down,
+                                             int32_t max_wg);
+
 /* Frees the host-side context and its profiling events (never the caller's
  * device buffers). */
 MOE_API void moe_destroy(moe_ctx *ctx);

@@ -27,7 +27,8 @@ EXPORTED = ["moe_weight_bytes", "moe_workspace_bytes", "moe_workspace_map", "moe
             "moe_load_expert",
             "moe_load_router", "moe_route", "moe_forward", "moe_forward_static",
             "moe_forward_stack",
-            "moe_intermediates", "moe_profile_enable", "moe_profile_read", "moe_destroy",
+            "moe_intermediates", "moe_profile_enable", "moe_profile_read",
+            "moe_profile_gemm_timeline", "moe_destroy",
             "moe_last_error", "moe_status_string", "moe_diag_stream_read"]
 
 KERNEL_KINDS = ["router", "route", "decode_gateup", "decode_down", "gemm_gateup", "gemm_down",
@@ -87,6 +88,7 @@ def lib():
         L.moe_intermediates.argtypes = [P, ctypes.POINTER(P), ctypes.POINTER(P)]
         L.moe_profile_enable.argtypes = [P, I]
         L.moe_profile_read.argtypes = [P, P, P, P]
+        L.moe_profile_gemm_timeline.argtypes = [P, P, P, I]
         L.moe_destroy.argtypes = [P]
         L.moe_destroy.restype = None
         L.moe_last_error.argtypes = [P]
@@ -96,7 +98,7 @@ def lib():
         L.moe_diag_stream_read.argtypes = [P, ctypes.c_uint64, P, P]
         for fn in ("moe_init", "moe_load_expert", "moe_load_router", "moe_route", "moe_forward",
                    "moe_forward_static", "moe_forward_stack", "moe_intermediates", "moe_profile_enable",
-                   "moe_profile_read", "moe_diag_stream_read"):
+                   "moe_profile_read", "moe_profile_gemm_timeline", "moe_diag_stream_read"):
             getattr(L, fn).restype = ctypes.c_int
         _lib = L
     return _lib
@@ -195,6 +197,12 @@ def moe_profile_read(ctx):
     dropped = ctypes.c_int64()
     _check(ctx, lib().moe_profile_read(ctx, ms, cnt, ctypes.byref(dropped)))
     return {k: (ms[i], cnt[i]) for i, k in enumerate(KERNEL_KINDS)}, dropped.value
+
+
+def moe_profile_gemm_timeline(ctx, gateup_ptr, down_ptr, max_wg: int):
+    """Per-workgroup GEMM timelines into two uint64 [max_wg][8] device
+    buffers (0 / None turns it off); see include/moe.h for the fields."""
+    _check(ctx, lib().moe_profile_gemm_timeline(ctx, gateup_ptr, down_ptr, max_wg))
 
 
 def moe_destroy(ctx):
@@ -363,22 +371,42 @@ class MoeLayer:
         return out
 
 
-def _copy_dev(dst_ptr: int, src_ptr: int, nbytes: int):
-    """Device-to-device copy through the HIP runtime (read-back helper)."""
+_hip = None
+HIP_ATTR_WALL_CLOCK_RATE = 10019   # hipDeviceAttributeWallClockRate (kHz)
+
+
+def _hip_runtime():
+    """The HIP runtime already mapped into this process (torch's)."""
     global _hip
-    try:
-        _hip
-    except NameError:
-        # the HIP runtime already mapped into this process (torch's)
+    if _hip is None:
+        lib()
         path = "libamdhip64.so"
         with open(f"/proc/{os.getpid()}/maps") as fh:
             for ln in fh:
                 if "libamdhip64" in ln and ln.split()[-1].startswith("/"):
                     path = ln.split()[-1]
                     break
-        _hip = ctypes.CDLL(path)
-        _hip.hipMemcpy.argtypes = [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_size_t, ctypes.c_int]
-        _hip.hipMemcpy.restype = ctypes.c_int
-    rc = _hip.hipMemcpy(ctypes.c_void_p(dst_ptr), ctypes.c_void_p(src_ptr), nbytes, 3)
+        h = ctypes.CDLL(path)
+        h.hipMemcpy.argtypes = [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_size_t, ctypes.c_int]
+        h.hipMemcpy.restype = ctypes.c_int
+        h.hipDeviceGetAttribute.argtypes = [ctypes.POINTER(ctypes.c_int), ctypes.c_int, ctypes.c_int]
+        h.hipDeviceGetAttribute.restype = ctypes.c_int
+        _hip = h
+    return _hip
+
+
+def _copy_dev(dst_ptr: int, src_ptr: int, nbytes: int):
+    """Device-to-device copy through the HIP runtime (read-back helper)."""
+    rc = _hip_runtime().hipMemcpy(ctypes.c_void_p(dst_ptr), ctypes.c_void_p(src_ptr), nbytes, 3)
     if rc != 0:
         raise RuntimeError(f"hipMemcpy failed: {rc}")
+
+
+def wall_clock_hz(device: int = 0) -> float:
+    """Rate of the constant counter the GEMM timeline's [0], [1] fields read
+    (hipDeviceAttributeWallClockRate)."""
+    v = ctypes.c_int()
+    rc = _hip_runtime().hipDeviceGetAttribute(ctypes.byref(v), HIP_ATTR_WALL_CLOCK_RATE, device)
+    if rc != 0:
+        raise RuntimeError(f"hipDeviceGetAttribute failed: {rc}")
+    return v.value * 1e3

@@ -145,6 +145,9 @@ struct moe_ctx {
     std::vector<hipEvent_t> prof_events;   // 2 per launch slot
     std::vector<int> prof_kinds;           // kind of each recorded launch
     int64_t prof_dropped;
+    uint64_t* tl_gateup;   // GEMM timelines (moe_profile_gemm_timeline), or NULL
+    uint64_t* tl_down;
+    int tl_max;
     // the routing that the last moe_route returned (moe_forward accepts it
     // while nothing has overwritten or outdated it)
     bool route_valid;
@@ -294,11 +297,14 @@ moe_status run_experts(moe_ctx* ctx, const WsView& ws, int layer, const uint16_t
         a.f = c.ffn_dim;
         a.e_begin = c.expert_begin;
         a.T = T;
+        a.max_stamps = ctx->tl_max;
         const int tile_rows = moe_prefill_tile_rows();
         const int kl = std::min(c.top_k, c.n_local_experts);
         a.max_tiles = (T * kl + tile_rows - 1) / tile_rows + c.n_local_experts;
+        a.stamps = ctx->tl_gateup;
         e = timed(ctx, MOE_K_GEMM_GATEUP, s, [&] { return moe_launch_gemm_gateup(&a, s); });
         if (e != hipSuccess) return hip_fail(ctx, e, "grouped GEMM gate/up kernel launch");
+        a.stamps = ctx->tl_down;
         e = timed(ctx, MOE_K_GEMM_DOWN, s, [&] { return moe_launch_gemm_down(&a, s); });
         if (e != hipSuccess) return hip_fail(ctx, e, "grouped GEMM down kernel launch");
     }
@@ -414,6 +420,8 @@ moe_status moe_init(const moe_config* cfg, void* weight_arena, void* workspace, 
     c->route_x = nullptr;
     c->prof_on = false;
     c->prof_dropped = 0;
+    c->tl_gateup = c->tl_down = nullptr;
+    c->tl_max = 0;
     *out = c;
     return MOE_OK;
 }
@@ -648,6 +656,19 @@ moe_status moe_profile_enable(moe_ctx* ctx, int32_t max_launches)
     }
     ctx->prof_kinds.reserve(max_launches);
     ctx->prof_on = true;
+    return MOE_OK;
+}
+
+moe_status moe_profile_gemm_timeline(moe_ctx* ctx, uint64_t* gateup, uint64_t* down,
+                                     int32_t max_wg)
+{
+    if (!ctx) return MOE_E_ARG;
+    if (max_wg < 0) return fail(ctx, MOE_E_ARG, "max_wg is negative");
+    if ((gateup && misaligned(gateup)) || (down && misaligned(down)))
+        return fail(ctx, MOE_E_ALIGN, "timeline buffers must be 16-byte aligned");
+    ctx->tl_gateup = max_wg ? gateup : nullptr;
+    ctx->tl_down = max_wg ? down : nullptr;
+    ctx->tl_max = max_wg;
     return MOE_OK;
 }
 

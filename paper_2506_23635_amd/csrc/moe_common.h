@@ -111,6 +111,8 @@ struct GemmArgs {
     const int32_t* n_tiles;   // [1]
     int d, f, e_begin, max_tiles;
     int T;                    // tokens of the call (rows of x)
+    uint64_t* stamps;         // per-workgroup timeline [max_stamps][8], or NULL (measurement)
+    int max_stamps;
 };
 
 }  // namespace moe

@@ -391,7 +391,35 @@ __global__ __launch_bounds__(kThreads) void gemm_kernel(GemmArgs a)
     const int logical = (blockIdx.x % kXcds) * per_xcd + blockIdx.x / kXcds;
     const int ft = logical / a.max_tiles, tt = logical % a.max_tiles;
     if (ft >= n_ftiles || tt >= *a.n_tiles) return;
+    // measurement only (a.stamps set by moe_profile_gemm_timeline): the
+    // constant 100 MHz counter and the shader-clock counter around the tile
+    const bool stamp = a.stamps != nullptr && (int)blockIdx.x < a.max_stamps;
+    uint64_t r0 = 0, c0 = 0;
+    if (stamp) {
+        r0 = __builtin_amdgcn_s_memrealtime();
+        c0 = __builtin_amdgcn_s_memtime();
+    }
     process_tile<kMode>(a, ft, tt, lds);
+    if (stamp) {
+        __syncthreads();
+        if (threadIdx.x == 0) {
+            const uint64_t r1 = __builtin_amdgcn_s_memrealtime();
+            const uint64_t c1 = __builtin_amdgcn_s_memtime();
+            uint32_t hw, xcc;
+            asm volatile("s_getreg_b32 %0, hwreg(HW_REG_HW_ID)" : "=s"(hw));
+            asm volatile("s_getreg_b32 %0, hwreg(HW_REG_XCC_ID)" : "=s"(xcc));
+            const int e = a.tiles[2 * tt], row0 = a.tiles[2 * tt + 1];
+            const int rows = min(row0 + BN, a.offsets[e + 1]) - row0;
+            uint64_t* out = a.stamps + (uint64_t)blockIdx.x * 8;
+            out[0] = r0;
+            out[1] = r1;
+            out[2] = c0;
+            out[3] = c1;
+            out[4] = (uint64_t)hw | ((uint64_t)xcc << 32);
+            out[5] = (uint64_t)ft | ((uint64_t)tt << 16) | ((uint64_t)rows << 32) |
+                     ((uint64_t)e << 48);
+        }
+    }
 }
 
 }  // namespace moe

@@ -323,6 +323,38 @@ def test_partial_f32_shares(torch_mod, T):
     assert np.all(np.abs(total - full["y64"]) <= bound + 1e-12 * np.abs(full["y64"]))
 
 
+def test_gemm_timeline_records_and_changes_nothing(torch_mod, tiny_layer):
+    """moe_profile_gemm_timeline (measurement): outputs are bit-identical with
+    it on, every workgroup with a tile records increasing counters and its
+    tile, the rows of each token tile add up to the routing's rows once per
+    feature tile, and turning it off stops the recording."""
+    torch = torch_mod
+    wl = TINY.with_(T=300)
+    x_t, _ = x_device(wl)
+    before = _forward(torch, tiny_layer, x_t)
+    n = 512
+    bufs = [torch.zeros(n * 8, dtype=torch.int64, device="cuda") for _ in range(2)]
+    moe.moe_profile_gemm_timeline(tiny_layer.ctx, bufs[0].data_ptr(), bufs[1].data_ptr(), n)
+    y = _forward(torch, tiny_layer, x_t)
+    moe.moe_profile_gemm_timeline(tiny_layer.ctx, None, None, 0)
+    assert np.array_equal(y, before)
+    rt = tiny_layer.routing_tensors(tiny_layer.route(0, x_t))
+    rows = int(rt["offsets"][-1])
+    for buf, n_ft in ((bufs[0], 2 * wl.f // 256), (bufs[1], wl.d // 256)):
+        t = buf.cpu().numpy().view(np.uint64).reshape(n, 8)
+        live = t[t[:, 1] > 0]
+        assert len(live) > 0
+        assert np.all(live[:, 1] >= live[:, 0]) and np.all(live[:, 3] > live[:, 2])
+        r = ((live[:, 5] >> 32) & 0xFFFF).astype(np.int64)
+        ft = (live[:, 5] & 0xFFFF).astype(np.int64)
+        assert np.all((r > 0) & (r <= 256)) and np.all(ft < n_ft)
+        assert int(r.sum()) == rows * n_ft
+    for b in bufs:
+        b.zero_()
+    _forward(torch, tiny_layer, x_t)
+    assert not bool(bufs[0].any()) and not bool(bufs[1].any())
+
+
 def test_routing_validity_rules(torch_mod):
     """moe_forward accepts a routing only while it is the current result of
     the last moe_route for that layer, T and x: an internal re-route, a stack
