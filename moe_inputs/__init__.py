@@ -31,6 +31,13 @@ KIND_BIAS = 3
 KIND_GATE = 4
 KIND_UP = 5
 KIND_DOWN = 6
+# attention block inputs
+KIND_ATTN_X = 7
+KIND_GAMMA = 8
+KIND_WQKV = 9
+KIND_WO = 10
+KIND_KCACHE = 11
+KIND_VCACHE = 12
 
 # sd of z = 2*S - 8*65535 where S is a sum of eight uniform 16-bit integers
 _SD_Z = 2.0 * math.sqrt(8.0 * (65536.0 ** 2 - 1.0) / 12.0)
@@ -236,4 +243,71 @@ WORKLOADS = {
     # 32 chained layers, all 16 experts resident, 4 decode tokens
     "stack": Workload("stack", T=4, d=DBRX_D, f=DBRX_F, E=16, k=4, sigma_w=0.006,
                       n_layers=32),
+}
+
+
+@dataclass(frozen=True)
+class AttnWorkload:
+    """One synthetic self-attention workload: T new tokens at positions
+    pos0 .. pos0+T-1 against a key/value cache holding positions 0 .. pos0-1.
+    Shapes follow Table tab:vars (D_embed 6144, D_qkv_hidden 8192 = 48 query
+    heads + 8 key + 8 value heads of 128); the head split, the rotary base and
+    the norm epsilon are the readings the oracle documents."""
+    name: str
+    T: int
+    pos0: int
+    d: int
+    n_heads: int
+    n_kv: int
+    hd: int
+    max_seq: int
+    theta: float = 5e5
+    eps: float = 1e-5
+    sigma_x: float = 1.0
+    sigma_qkv: float = 0.02     # fused query/key/value projection weights
+    sigma_o: float = 0.006      # output projection weights
+    sigma_gamma: float = 0.1    # norm scale = 1 + N(0, sigma_gamma)
+    sigma_cache: float = 1.5    # cached keys and values of earlier positions
+    n_layers: int = 1
+    seed: int = 0
+
+    @property
+    def nqkv(self) -> int:
+        return (self.n_heads + 2 * self.n_kv) * self.hd
+
+    def with_(self, **kw) -> "AttnWorkload":
+        from dataclasses import replace
+        return replace(self, **kw)
+
+    def x(self, layer: int = 0) -> np.ndarray:
+        return gen_bf16(self.seed, stream_id(KIND_ATTN_X, layer), (self.T, self.d), self.sigma_x)
+
+    def gamma(self, layer: int = 0) -> np.ndarray:
+        g = gen_f32(self.seed, stream_id(KIND_GAMMA, layer), (self.d,), self.sigma_gamma)
+        return (np.float32(1.0) + g).astype(np.float32)
+
+    def wqkv(self, layer: int = 0) -> np.ndarray:
+        return gen_bf16(self.seed, stream_id(KIND_WQKV, layer), (self.d, self.nqkv), self.sigma_qkv)
+
+    def wo(self, layer: int = 0) -> np.ndarray:
+        return gen_bf16(self.seed, stream_id(KIND_WO, layer), (self.n_heads * self.hd, self.d),
+                        self.sigma_o)
+
+    def cache_prefix(self, layer: int = 0):
+        """Keys and values of positions 0 .. pos0-1, bf16 bits [pos0, n_kv, hd]
+        (position-major)."""
+        shape = (self.pos0, self.n_kv, self.hd)
+        return (gen_bf16(self.seed, stream_id(KIND_KCACHE, layer), shape, self.sigma_cache),
+                gen_bf16(self.seed, stream_id(KIND_VCACHE, layer), shape, self.sigma_cache))
+
+
+ATTN_WORKLOADS = {
+    # small parity case: 4 query heads sharing 2 key/value heads of 64, 4 new
+    # tokens after 29 cached positions
+    "attn_tiny": AttnWorkload("attn_tiny", T=4, pos0=29, d=256, n_heads=4, n_kv=2, hd=64,
+                              max_seq=256, theta=1e4),
+    # one decode token of the DBRX block after a 2047-token context (the
+    # paper's long-prompt workload has 2000 input tokens)
+    "attn_decode": AttnWorkload("attn_decode", T=1, pos0=2047, d=6144, n_heads=48, n_kv=8,
+                                hd=128, max_seq=4096),
 }

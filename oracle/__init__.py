@@ -1,4 +1,5 @@
-"""TEST INFRASTRUCTURE ONLY: ctypes binding of the fp64 CPU oracle.
+"""TEST INFRASTRUCTURE ONLY: ctypes binding of the fp64 CPU oracles (the MoE
+layer in moe_oracle.c, the self-attention block in attn_oracle.c).
 
 Only the test-suite, the smoke check and the benchmark's CPU-baseline leg may
 import this package.  The product library never loads it, and it never loads
@@ -44,6 +45,14 @@ def lib():
         L.oracle_layer.argtypes = [_i] * 7 + [_p] * 11
         L.oracle_layer_dense.argtypes = [_i] * 5 + [_p] * 7
         L.oracle_residual_add.argtypes = [_p, _p, _p, ctypes.c_int64]
+        L.oracle_layernorm.argtypes = [_i, _i, _p, _p, ctypes.c_double, _p]
+        L.oracle_rope.argtypes = [_i, _i, _p, _p, ctypes.c_double, _p]
+        L.oracle_attention_core.argtypes = [_i] * 5 + [_p] * 5
+        L.oracle_attention_block.argtypes = ([_i] * 6 + [_p, _p, ctypes.c_double, ctypes.c_double] +
+                                             [_p] * 11)
+        for fn in ("oracle_layernorm", "oracle_rope", "oracle_attention_core",
+                   "oracle_attention_block"):
+            getattr(L, fn).restype = ctypes.c_int
         for fn in ("oracle_router_logits", "oracle_route_from_logits", "oracle_permutation",
                    "oracle_expert_glu", "oracle_layer_with_routing",
                    "oracle_layer_with_routing_ex", "oracle_layer",
@@ -245,4 +254,74 @@ def residual_add(x, y) -> np.ndarray:
     assert x.shape == y.shape
     out = np.empty(x.shape, dtype=np.uint16)
     lib().oracle_residual_add(px, py, out.ctypes.data, x.size)
+    return out
+
+
+# ------------------------------------------------------------ attention --
+# Layouts: x bf16 [T, d]; gamma fp32 [d]; wqkv bf16 [d, (H + 2 G) hd];
+# wo bf16 [H hd, d]; k/v caches bf16 [L, G, hd] (position-major), H query
+# heads, G key/value heads.
+
+
+def layernorm(x, gamma, eps: float) -> np.ndarray:
+    x, px = _c(x, np.uint16)
+    gamma, pg = _c(gamma, np.float32)
+    T, d = x.shape
+    h = np.empty((T, d), dtype=np.uint16)
+    _check(lib().oracle_layernorm(T, d, px, pg, float(eps), h.ctypes.data), "layernorm")
+    return h
+
+
+def rope(v, pos, theta: float) -> np.ndarray:
+    """Rotary encoding of head vectors v [n, hd] (fp64) at positions pos [n]."""
+    v, pv = _c(v, np.float64)
+    pos, pp = _c(pos, np.int32)
+    n, hd = v.shape
+    out = np.empty_like(v)
+    _check(lib().oracle_rope(n, hd, pv, pp, float(theta), out.ctypes.data), "rope")
+    return out
+
+
+def attention_core(q, k_cache, v_cache, pos0: int):
+    """Causal grouped-query attention of q [T, H, hd] (bf16 bits) over caches
+    [L, G, hd] holding positions 0 .. pos0+T-1.  Returns (attn bf16
+    [T, H*hd], attn64 fp64 [T, H*hd])."""
+    q, pq = _c(q, np.uint16)
+    k_cache, pk = _c(k_cache, np.uint16)
+    v_cache, pv = _c(v_cache, np.uint16)
+    T, H, hd = q.shape
+    G = k_cache.shape[1]
+    assert k_cache.shape[0] >= pos0 + T and v_cache.shape == k_cache.shape
+    out = np.empty((T, H * hd), dtype=np.uint16)
+    out64 = np.empty((T, H * hd), dtype=np.float64)
+    _check(lib().oracle_attention_core(T, H, G, hd, pos0, pq, pk, pv, out.ctypes.data,
+                                       out64.ctypes.data), "attention_core")
+    return out, out64
+
+
+def attention_block(x, gamma, wqkv, wo, k_cache, v_cache, pos0: int, n_heads: int, n_kv: int,
+                    eps: float, theta: float):
+    """The block on x [T, d] at positions pos0 ..; k_cache / v_cache
+    [L, G, hd] bf16 bits are updated in place (positions pos0 .. pos0+T-1).
+    Returns a dict of h, qkv64, q, attn, o64, y64, y (see attn_oracle.c)."""
+    x, px = _c(x, np.uint16)
+    gamma, pg = _c(gamma, np.float32)
+    wqkv, pq = _c(wqkv, np.uint16)
+    wo, pw = _c(wo, np.uint16)
+    assert k_cache.dtype == np.uint16 and v_cache.dtype == np.uint16
+    assert k_cache.flags.c_contiguous and v_cache.flags.c_contiguous
+    T, d = x.shape
+    hd = wo.shape[0] // n_heads
+    nqkv = (n_heads + 2 * n_kv) * hd
+    assert wqkv.shape == (d, nqkv) and wo.shape == (n_heads * hd, d)
+    assert k_cache.shape[1:] == (n_kv, hd) and k_cache.shape[0] >= pos0 + T
+    out = {"h": np.empty((T, d), np.uint16), "qkv64": np.empty((T, nqkv), np.float64),
+           "q": np.empty((T, n_heads * hd), np.uint16), "attn": np.empty((T, n_heads * hd), np.uint16),
+           "o64": np.empty((T, d), np.float64), "y64": np.empty((T, d), np.float64),
+           "y": np.empty((T, d), np.uint16)}
+    _check(lib().oracle_attention_block(
+        T, d, n_heads, n_kv, hd, pos0, px, pg, float(eps), float(theta), pq, pw,
+        k_cache.ctypes.data, v_cache.ctypes.data, out["h"].ctypes.data, out["qkv64"].ctypes.data,
+        out["q"].ctypes.data, out["attn"].ctypes.data, out["o64"].ctypes.data,
+        out["y64"].ctypes.data, out["y"].ctypes.data), "attention_block")
     return out

@@ -3,7 +3,7 @@ the fp64 oracle and the host input generator are rebuilt with
 -fsanitize=address,undefined (errors fatal) and driven, in a child Python
 process that preloads the ASan runtime, through every oracle entry point
 on the tiny and wide configurations, an expert-parallel share, the dense
-form and the stacked residual.  The child must exit cleanly and produce the
+form, the stacked residual and the small attention block.  The child must exit cleanly and produce the
 same bits as the regular builds."""
 import hashlib
 import os
@@ -41,6 +41,17 @@ def run():
         y2 = oracle.residual_add(x, full["y"])
         for a in (x, lg, idx, w, full["y64"], full["y"], share["y64"], dense, y2):
             h.update(np.ascontiguousarray(a).tobytes())
+    # the attention block: T new tokens after a cached prefix
+    aw = mi.ATTN_WORKLOADS["attn_tiny"]
+    k0, v0 = aw.cache_prefix()
+    kc = np.zeros((aw.max_seq, aw.n_kv, aw.hd), np.uint16)
+    vc = np.zeros_like(kc)
+    kc[:aw.pos0], vc[:aw.pos0] = k0, v0
+    r = oracle.attention_block(aw.x(), aw.gamma(), aw.wqkv(), aw.wo(), kc, vc, aw.pos0,
+                               aw.n_heads, aw.n_kv, aw.eps, aw.theta)
+    for key in ("h", "qkv64", "q", "attn", "o64", "y64", "y"):
+        h.update(np.ascontiguousarray(r[key]).tobytes())
+    h.update(kc.tobytes())
     return h.hexdigest()
 
 
@@ -53,7 +64,8 @@ def _build_sanitized(tmp):
     ora = os.path.join(tmp, "libmoe_oracle_san.so")
     gen = os.path.join(tmp, "libmoe_inputs_host_san.so")
     subprocess.run(["gcc", "-std=c11", "-fno-fast-math", "-ffp-contract=off", "-fopenmp", "-fPIC",
-                    "-shared", *SAN, "-o", ora, os.path.join(ROOT, "oracle", "moe_oracle.c"), "-lm"],
+                    "-shared", *SAN, "-o", ora, os.path.join(ROOT, "oracle", "moe_oracle.c"),
+                    os.path.join(ROOT, "oracle", "attn_oracle.c"), "-lm"],
                    check=True)
     subprocess.run(["gcc", "-std=c11", "-ffp-contract=off", "-fopenmp", "-fPIC", "-shared", *SAN,
                     "-o", gen, os.path.join(ROOT, "moe_inputs", "gen_host.c")], check=True)
