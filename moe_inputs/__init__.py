@@ -305,7 +305,7 @@ ATTN_WORKLOADS = {
     # small parity case: 4 query heads sharing 2 key/value heads of 64, 4 new
     # tokens after 29 cached positions
     "attn_tiny": AttnWorkload("attn_tiny", T=4, pos0=29, d=256, n_heads=4, n_kv=2, hd=64,
-                              max_seq=256, theta=1e4),
+                              max_seq=512, theta=1e4),
     # one decode token of the DBRX block after a 2047-token context (the
     # paper's long-prompt workload has 2000 input tokens)
     "attn_decode": AttnWorkload("attn_decode", T=1, pos0=2047, d=6144, n_heads=48, n_kv=8,

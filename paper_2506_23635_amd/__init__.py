@@ -29,7 +29,13 @@ EXPORTED = ["moe_weight_bytes", "moe_workspace_bytes", "moe_workspace_map", "moe
             "moe_forward_stack",
             "moe_intermediates", "moe_profile_enable", "moe_profile_read",
             "moe_profile_gemm_timeline", "moe_destroy",
-            "moe_last_error", "moe_status_string", "moe_diag_stream_read"]
+            "moe_last_error", "moe_status_string", "moe_diag_stream_read",
+            # include/attn.h
+            "attn_weight_bytes", "attn_cache_bytes", "attn_workspace_bytes", "attn_init",
+            "attn_load_layer", "attn_forward", "attn_intermediates", "attn_profile_enable",
+            "attn_profile_read", "attn_destroy", "attn_last_error"]
+
+ATTN_KERNEL_KINDS = ["norm", "qkv", "rope", "score", "combine", "out", "pack"]
 
 KERNEL_KINDS = ["router", "route", "decode_gateup", "decode_down", "gemm_gateup", "gemm_down",
                 "combine", "pack"]
@@ -49,6 +55,14 @@ class MoeRouting(ctypes.Structure):
                 ("offsets", ctypes.c_void_p), ("pair_row", ctypes.c_void_p),
                 ("row_token", ctypes.c_void_p), ("T", ctypes.c_int32),
                 ("layer", ctypes.c_int32)]
+
+
+class AttnConfig(ctypes.Structure):
+    _fields_ = [("d_model", ctypes.c_int32), ("n_heads", ctypes.c_int32),
+                ("n_kv_heads", ctypes.c_int32), ("head_dim", ctypes.c_int32),
+                ("n_layers", ctypes.c_int32), ("max_seq", ctypes.c_int32),
+                ("max_tokens", ctypes.c_int32), ("rope_theta", ctypes.c_float),
+                ("norm_eps", ctypes.c_float), ("flags", ctypes.c_int32)]
 
 
 class MoeError(RuntimeError):
@@ -96,6 +110,23 @@ def lib():
         L.moe_status_string.argtypes = [ctypes.c_int]
         L.moe_status_string.restype = ctypes.c_char_p
         L.moe_diag_stream_read.argtypes = [P, ctypes.c_uint64, P, P]
+        acfg = ctypes.POINTER(AttnConfig)
+        for fn in ("attn_weight_bytes", "attn_cache_bytes", "attn_workspace_bytes"):
+            getattr(L, fn).argtypes = [acfg]
+            getattr(L, fn).restype = ctypes.c_size_t
+        L.attn_init.argtypes = [acfg, P, P, P, ctypes.POINTER(P)]
+        L.attn_load_layer.argtypes = [P, I, P, P, P, I, P]
+        L.attn_forward.argtypes = [P, I, P, P, I, I, P]
+        L.attn_intermediates.argtypes = [P] + [ctypes.POINTER(P)] * 5
+        L.attn_profile_enable.argtypes = [P, I]
+        L.attn_profile_read.argtypes = [P, P, P, P]
+        L.attn_destroy.argtypes = [P]
+        L.attn_destroy.restype = None
+        L.attn_last_error.argtypes = [P]
+        L.attn_last_error.restype = ctypes.c_char_p
+        for fn in ("attn_init", "attn_load_layer", "attn_forward", "attn_intermediates",
+                   "attn_profile_enable", "attn_profile_read"):
+            getattr(L, fn).restype = ctypes.c_int
         for fn in ("moe_init", "moe_load_expert", "moe_load_router", "moe_route", "moe_forward",
                    "moe_forward_static", "moe_forward_stack", "moe_intermediates", "moe_profile_enable",
                    "moe_profile_read", "moe_profile_gemm_timeline", "moe_diag_stream_read"):
@@ -410,3 +441,152 @@ def wall_clock_hz(device: int = 0) -> float:
     if rc != 0:
         raise RuntimeError(f"hipDeviceGetAttribute failed: {rc}")
     return v.value * 1e3
+
+
+# ------------------------------------------------------- attention block --
+
+def _acheck(ctx, status: int):
+    if status != MOE_OK:
+        raise MoeError(status, lib().attn_last_error(ctx).decode())
+
+
+def make_attn_config(d_model, n_heads, n_kv_heads, head_dim, n_layers=1, max_seq=4096,
+                     max_tokens=16, rope_theta=5e5, norm_eps=1e-5, flags=0) -> AttnConfig:
+    return AttnConfig(d_model, n_heads, n_kv_heads, head_dim, n_layers, max_seq, max_tokens,
+                      rope_theta, norm_eps, flags)
+
+
+def attn_weight_bytes(cfg: AttnConfig) -> int:
+    return int(lib().attn_weight_bytes(ctypes.byref(cfg)))
+
+
+def attn_cache_bytes(cfg: AttnConfig) -> int:
+    return int(lib().attn_cache_bytes(ctypes.byref(cfg)))
+
+
+def attn_workspace_bytes(cfg: AttnConfig) -> int:
+    return int(lib().attn_workspace_bytes(ctypes.byref(cfg)))
+
+
+def attn_init(cfg: AttnConfig, arena_ptr: int, cache_ptr: int, workspace_ptr: int) -> int:
+    out = ctypes.c_void_p()
+    _acheck(None, lib().attn_init(ctypes.byref(cfg), arena_ptr, cache_ptr, workspace_ptr,
+                                  ctypes.byref(out)))
+    return out.value
+
+
+def attn_load_layer(ctx, layer, gamma_ptr, wqkv_ptr, wo_ptr, src_on_device, stream=0):
+    _acheck(ctx, lib().attn_load_layer(ctx, layer, gamma_ptr, wqkv_ptr, wo_ptr, src_on_device,
+                                       stream))
+
+
+def attn_forward(ctx, layer, x_ptr, y_ptr, T, pos0, stream=0):
+    _acheck(ctx, lib().attn_forward(ctx, layer, x_ptr, y_ptr, T, pos0, stream))
+
+
+def attn_intermediates(ctx):
+    ptrs = [ctypes.c_void_p() for _ in range(5)]
+    _acheck(ctx, lib().attn_intermediates(ctx, *[ctypes.byref(p) for p in ptrs]))
+    return [p.value for p in ptrs]
+
+
+def attn_profile_enable(ctx, max_launches: int):
+    _acheck(ctx, lib().attn_profile_enable(ctx, max_launches))
+
+
+def attn_profile_read(ctx):
+    n = len(ATTN_KERNEL_KINDS)
+    ms = (ctypes.c_double * n)()
+    cnt = (ctypes.c_int64 * n)()
+    dropped = ctypes.c_int64()
+    _acheck(ctx, lib().attn_profile_read(ctx, ms, cnt, ctypes.byref(dropped)))
+    return {k: (ms[i], cnt[i]) for i, k in enumerate(ATTN_KERNEL_KINDS)}, dropped.value
+
+
+class AttnLayer:
+    """Owns an attention context plus its torch-allocated weight arena, key/value
+    cache and workspace on one GPU (argument marshalling only)."""
+
+    def __init__(self, cfg: AttnConfig, device="cuda", arena=None, cache=None, workspace=None):
+        import torch
+        self.torch = torch
+        self.cfg = cfg
+        self.device = torch.device(device)
+        if self.device.index is None:
+            self.device = torch.device("cuda", torch.cuda.current_device())
+        wb, cb, sb = attn_weight_bytes(cfg), attn_cache_bytes(cfg), attn_workspace_bytes(cfg)
+        if not (wb and cb and sb):
+            raise MoeError(-2, "invalid attention config")
+
+        def buf(t, n, name):
+            if t is None:
+                return torch.empty(n, dtype=torch.uint8, device=self.device)
+            _tensor_ptr(t, name, n, (torch.uint8,), self.device)
+            return t
+        self.arena = buf(arena, wb, "arena")
+        self.cache = buf(cache, cb, "cache")
+        self.workspace = buf(workspace, sb, "workspace")
+        self.ctx = attn_init(cfg, self.arena.data_ptr(), self.cache.data_ptr(),
+                             self.workspace.data_ptr())
+
+    @property
+    def stream(self) -> int:
+        return self.torch.cuda.current_stream(self.device).cuda_stream
+
+    def close(self):
+        if getattr(self, "ctx", None):
+            lib().attn_destroy(self.ctx)
+            self.ctx = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+    def cache_views(self, layer):
+        """(K, V) of a layer as bf16-bit int16 views [n_kv_heads, max_seq, head_dim]."""
+        c = self.cfg
+        per = c.n_kv_heads * c.max_seq * c.head_dim
+        allc = self.cache.view(self.torch.int16).view(c.n_layers, 2, per)
+        shape = (c.n_kv_heads, c.max_seq, c.head_dim)
+        return allc[layer, 0].view(shape), allc[layer, 1].view(shape)
+
+    def load_layer(self, layer, gamma, wqkv, wo):
+        c, bf = self.cfg, _bf16_types(self.torch)
+        on_dev = wqkv.is_cuda
+        if gamma.is_cuda != on_dev or wo.is_cuda != on_dev:
+            raise MoeError(-1, "weights must be all on the GPU or all on the host")
+        dev = self.device if on_dev else self.torch.device("cpu")
+        nq = c.n_heads * c.head_dim
+        nqkv = (c.n_heads + 2 * c.n_kv_heads) * c.head_dim
+        attn_load_layer(self.ctx, layer,
+                        _tensor_ptr(gamma, "gamma", c.d_model, (self.torch.float32,), dev),
+                        _tensor_ptr(wqkv, "wqkv", c.d_model * nqkv, bf, dev),
+                        _tensor_ptr(wo, "wo", nq * c.d_model, bf, dev), int(on_dev),
+                        self.stream if on_dev else 0)
+
+    def forward(self, layer, x, y, pos0, T=None):
+        T = x.shape[0] if T is None else int(T)
+        n, bf = T * self.cfg.d_model, _bf16_types(self.torch)
+        attn_forward(self.ctx, layer, _tensor_ptr(x, "x", n, bf, self.device),
+                     _tensor_ptr(y, "y", n, bf, self.device), T, pos0, self.stream)
+
+    def intermediates(self, T):
+        """Copies of the last forward's h, qkv, q, a, o (numpy; bf16 as uint16)."""
+        import numpy as np
+        torch = self.torch
+        c = self.cfg
+        nq = c.n_heads * c.head_dim
+        nqkv = (c.n_heads + 2 * c.n_kv_heads) * c.head_dim
+        ptrs = attn_intermediates(self.ctx)
+        spec = [(c.d_model, torch.int16), (nqkv, torch.float32), (nq, torch.int16),
+                (nq, torch.int16), (c.d_model, torch.float32)]
+        out = []
+        torch.cuda.synchronize(self.device)
+        for ptr, (w, dt) in zip(ptrs, spec):
+            t = torch.empty((T, w), dtype=dt, device=self.device)
+            _copy_dev(t.data_ptr(), ptr, t.numel() * t.element_size())
+            a = t.cpu().numpy()
+            out.append(a.view(np.uint16) if dt == torch.int16 else a)
+        return dict(zip(["h", "qkv", "q", "a", "o"], out))

@@ -325,21 +325,6 @@ moe_status combine(moe_ctx* ctx, const WsView& ws, int T, uint16_t* y, float* y3
     return MOE_OK;
 }
 
-// Host-side prestacking of one [K][N] matrix into fragment tiles.
-void pack_host(const uint16_t* src, int K, int N, uint8_t* dst, int rt_mul, int rt_add)
-{
-    const uint64_t KT = (uint64_t)K / moe::kTileK;
-    for (int n = 0; n < N; ++n) {
-        const uint64_t rt = (uint64_t)(n / moe::kTileRows) * rt_mul + rt_add;
-        for (int k0 = 0; k0 < K; k0 += 8) {
-            const uint64_t kt = (uint64_t)k0 / moe::kTileK;
-            const int lane = ((k0 % moe::kTileK) / 8) * 16 + (n % moe::kTileRows);
-            uint16_t* p = reinterpret_cast<uint16_t*>(dst + moe::tile_offset(rt, kt, KT) + lane * 16);
-            for (int i = 0; i < 8; ++i) p[i] = src[(size_t)(k0 + i) * N + n];
-        }
-    }
-}
-
 // The static scratch of moe_forward_static: one array per GPU, held until
 // the process ends.  Host code never uses the array's name as an address
 // (on the host it is only a stand-in for the device symbol); the device
@@ -458,9 +443,9 @@ moe_status moe_load_expert(moe_ctx* ctx, int32_t layer, int32_t expert, const ui
         } catch (...) {
             return fail(ctx, MOE_E_ARG, "out of host memory for the host repack");
         }
-        pack_host(gate, d, f, tmp.data(), 2, 0);
-        pack_host(up, d, f, tmp.data(), 2, 1);
-        pack_host(down, f, d, tmp.data() + ctx->L.gu_bytes, 1, 0);
+        moe_pack_host(gate, d, f, tmp.data(), 2, 0);
+        moe_pack_host(up, d, f, tmp.data(), 2, 1);
+        moe_pack_host(down, f, d, tmp.data() + ctx->L.gu_bytes, 1, 0);
         hipError_t e = hipMemcpyAsync(dst, tmp.data(), tmp.size(), hipMemcpyHostToDevice, s);
         if (e == hipSuccess) e = hipStreamSynchronize(s);
         if (e != hipSuccess) return hip_fail(ctx, e, "host-to-device copy of packed expert");

@@ -121,6 +121,7 @@ struct GemmArgs {
 extern "C" {
 hipError_t moe_launch_pack(const uint16_t* src, int K, int N, void* dst, int rt_mul, int rt_add,
                            hipStream_t s);
+void moe_pack_host(const uint16_t* src, int K, int N, uint8_t* dst, int rt_mul, int rt_add);
 int moe_route_decode_ok(int T, int E, int k);
 int moe_route_decode_wgs(int d);
 hipError_t moe_launch_route_decode(const uint16_t* x, const float* wrT, const float* bias,
@@ -140,4 +141,20 @@ int moe_prefill_tile_rows();
 hipError_t moe_launch_combine(const float* O, const int32_t* pair_row, const float* topk_w, int T,
                               int d, int k, uint16_t* y, float* y32, uint16_t* x_residual,
                               hipStream_t s);
+}
+
+// Launchers of the attention-block kernels (attn.hip).
+extern "C" {
+hipError_t attn_launch_norm(const uint16_t* x, const float* gamma, int T, int d, float eps,
+                            uint16_t* h, hipStream_t s);
+hipError_t attn_launch_gemv(int out_mode, const void* w, const uint16_t* x, int T, int K, int N,
+                            float* y32, const uint16_t* res, uint16_t* y16, hipStream_t s);
+hipError_t attn_launch_rope(const float* qkv, uint16_t* q, uint16_t* kc, uint16_t* vc, int T,
+                            int H, int G, int hd, int max_seq, int pos0, double theta,
+                            hipStream_t s);
+int attn_chunks(int n_pos);
+int attn_part_stride(int hd);
+hipError_t attn_launch_attention(const uint16_t* q, const uint16_t* kc, const uint16_t* vc,
+                                 float* part, uint16_t* out, int T, int H, int G, int hd,
+                                 int max_seq, int pos0, int n_chunks_alloc, hipStream_t s);
 }

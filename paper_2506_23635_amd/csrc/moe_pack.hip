@@ -60,3 +60,19 @@ extern "C" hipError_t moe_launch_pack(const uint16_t* src, int K, int N, void* d
                        rt_add);
     return hipGetLastError();
 }
+
+// The same repack on the host, for weights that arrive in host memory.
+extern "C" void moe_pack_host(const uint16_t* src, int K, int N, uint8_t* dst, int rt_mul,
+                              int rt_add)
+{
+    const uint64_t KT = (uint64_t)K / moe::kTileK;
+    for (int n = 0; n < N; ++n) {
+        const uint64_t rt = (uint64_t)(n / moe::kTileRows) * rt_mul + rt_add;
+        for (int k0 = 0; k0 < K; k0 += 8) {
+            const uint64_t kt = (uint64_t)k0 / moe::kTileK;
+            const int lane = ((k0 % moe::kTileK) / 8) * 16 + (n % moe::kTileRows);
+            uint16_t* p = reinterpret_cast<uint16_t*>(dst + moe::tile_offset(rt, kt, KT) + lane * 16);
+            for (int i = 0; i < 8; ++i) p[i] = src[(size_t)(k0 + i) * N + n];
+        }
+    }
+}

@@ -10,14 +10,14 @@ import pytest
 import paper_2506_23635_amd as moe
 
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
-HEADER = os.path.join(ROOT, "include", "moe.h")
+HEADERS = [os.path.join(ROOT, "include", h) for h in ("moe.h", "attn.h")]
 
 E_ARG, E_SHAPE, E_ALIGN, E_CAPACITY, E_STATE = -1, -2, -3, -4, -5
 
 
 def declared_functions():
-    text = open(HEADER).read()
-    return sorted(set(re.findall(r"MOE_API\s+[\w\s\*]*?\b(moe_\w+)\s*\(", text)))
+    text = "".join(open(h).read() for h in HEADERS)
+    return sorted(set(re.findall(r"MOE_API\s+[\w\s\*]*?\b((?:moe|attn)_\w+)\s*\(", text)))
 
 
 def test_header_declares_the_boundary():
@@ -218,7 +218,71 @@ def test_layer_needs_a_gpu_device():
 
 
 def test_binding_constants_match_the_header():
-    text = open(HEADER).read()
+    text = open(HEADERS[0]).read()
     assert int(re.search(r"#define MOE_DIAG_MAX_WG (\d+)", text).group(1)) == moe.DIAG_MAX_WG
+    assert int(re.search(r"#define MOE_PARTIAL_F32 0x(\d+)", text).group(1), 16) == moe.MOE_PARTIAL_F32
     for name, value in moe.STATUS_NAMES.items():
         assert re.search(rf"\b{value}\s*=\s*{name}\b", text), value
+    def enum_body(src, name):
+        end = src.index("} %s;" % name)
+        return src[src.rindex("typedef enum {", 0, end):end]
+    regions = enum_body(text, "moe_ws_region")
+    names = [n.lower()[len("moe_ws_"):] for n in re.findall(r"\b(MOE_WS_\w+)", regions)]
+    assert names[:-1] == moe.WS_REGIONS and names[-1] == "count"
+    atext = open(HEADERS[1]).read()
+    kinds = enum_body(atext, "attn_kernel_kind")
+    knames = [n.lower()[len("attn_k_"):] for n in re.findall(r"\b(ATTN_K_\w+)", kinds)]
+    assert knames[:-1] == moe.ATTN_KERNEL_KINDS and knames[-1] == "count"
+
+
+def _attn_cfg(**kw):
+    base = dict(d_model=6144, n_heads=48, n_kv_heads=8, head_dim=128, n_layers=1, max_seq=4096,
+                max_tokens=16)
+    base.update(kw)
+    return moe.make_attn_config(**base)
+
+
+def test_attn_sizes():
+    cfg = _attn_cfg()
+    layer = 6144 * 4 + (6144 * 8192 + 6144 * 6144) * 2     # gamma, Wqkv, Wo
+    assert moe.attn_weight_bytes(cfg) == layer
+    assert moe.attn_cache_bytes(_attn_cfg(n_layers=3)) == 3 * 2 * 8 * 4096 * 128 * 2
+    assert moe.attn_workspace_bytes(cfg) > 16 * (6144 * 2 + 8192 * 4)
+
+
+@pytest.mark.parametrize("bad", [dict(d_model=200), dict(head_dim=96), dict(n_kv_heads=5),
+                                 dict(n_heads=64, n_kv_heads=4), dict(max_tokens=17),
+                                 dict(max_tokens=0), dict(max_seq=0), dict(n_layers=0),
+                                 dict(rope_theta=1.0), dict(norm_eps=-1.0), dict(flags=1),
+                                 dict(n_heads=3, n_kv_heads=1, head_dim=64)])
+def test_attn_bad_configs_rejected(bad):
+    # n_heads 64 over 4 key/value heads: 16 query heads share one, past the
+    # attention kernel's 8; 3 heads of 64: the output projection's K (192) is
+    # not a multiple of 256
+    cfg = _attn_cfg(**bad)
+    assert moe.attn_weight_bytes(cfg) == 0
+    out = ctypes.c_void_p()
+    assert moe.lib().attn_init(ctypes.byref(cfg), 4096, 8192, 16384, ctypes.byref(out)) == E_SHAPE
+    assert out.value is None and moe.lib().attn_last_error(None)
+
+
+def test_attn_validation_before_any_launch():
+    cfg = _attn_cfg(d_model=256, n_heads=4, n_kv_heads=2, head_dim=64, n_layers=2, max_seq=64,
+                    max_tokens=4)
+    L = moe.lib()
+    out = ctypes.c_void_p()
+    assert L.attn_init(ctypes.byref(cfg), 4096 + 16, 8192, 16384, ctypes.byref(out)) == E_ALIGN
+    assert L.attn_init(ctypes.byref(cfg), None, 8192, 16384, ctypes.byref(out)) == E_ARG
+    ctx = moe.attn_init(cfg, 1 << 20, 1 << 24, 1 << 26)
+    try:
+        assert L.attn_forward(ctx, 0, 4096, 4096, 1, 0, None) == E_STATE      # not loaded
+        assert L.attn_forward(ctx, 2, 4096, 4096, 1, 0, None) == E_ARG
+        assert L.attn_forward(ctx, 0, 4096, 4096, 5, 0, None) == E_CAPACITY   # T > max_tokens
+        assert L.attn_forward(ctx, 0, 4096, 4096, 2, 63, None) == E_CAPACITY  # past max_seq
+        assert L.attn_forward(ctx, 0, 4096, 4096, 1, -1, None) == E_ARG
+        assert L.attn_load_layer(ctx, 0, None, 4096, 4096, 1, None) == E_ARG
+        assert L.attn_load_layer(ctx, 0, 4096 + 4, 4096, 4096, 1, None) == E_ALIGN
+        assert L.attn_load_layer(ctx, 5, 4096, 4096, 4096, 1, None) == E_ARG
+        assert "range" in moe.lib().attn_last_error(ctx).decode()
+    finally:
+        L.attn_destroy(ctx)
