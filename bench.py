@@ -457,6 +457,86 @@ def gemm_timeline(layer, x):
     return out
 
 
+def attn_section(steps, warmup, n_rot=N_ROT):
+    """The DBRX self-attention block on one decode token after 2047 cached
+    positions (the paper's long-prompt workload has 2000 input tokens): layer
+    norm, fused projection (D_qkv_hidden 8192), rotary encoding and cache
+    append, attention over 2048 positions, output projection and residual.
+    n_rot independently seeded layers, step i on layer i % n_rot, so no
+    weight byte is re-read within 0.5 GB.  HBM bytes per step: Wqkv + Wo +
+    gamma + the keys and values of the 2048 positions + x and y."""
+    import numpy as np
+    import torch
+    import moe_inputs as mi
+    import paper_2506_23635_amd as moe
+    wl = mi.ATTN_WORKLOADS["attn_decode"]
+    cfg = moe.make_attn_config(wl.d, wl.n_heads, wl.n_kv, wl.hd, n_layers=n_rot,
+                               max_seq=wl.max_seq, max_tokens=16, rope_theta=wl.theta,
+                               norm_eps=wl.eps)
+    pool_reset()
+    layer = moe.AttnLayer(cfg, arena=pool_take(moe.attn_weight_bytes(cfg)),
+                          cache=pool_take(moe.attn_cache_bytes(cfg)),
+                          workspace=pool_take(moe.attn_workspace_bytes(cfg)))
+    s = layer.stream
+    stg = pool_take(wl.d * wl.nqkv * 2).view(torch.int16)
+    stg2 = pool_take(wl.n_heads * wl.hd * wl.d * 2).view(torch.int16)
+    for li in range(n_rot):
+        mi.gen_bf16_device(wl.seed, mi.stream_id(mi.KIND_WQKV, li), wl.d * wl.nqkv, wl.sigma_qkv,
+                           stg.data_ptr(), s)
+        mi.gen_bf16_device(wl.seed, mi.stream_id(mi.KIND_WO, li), wl.n_heads * wl.hd * wl.d,
+                           wl.sigma_o, stg2.data_ptr(), s)
+        layer.load_layer(li, torch.from_numpy(wl.gamma(li)).cuda(), stg, stg2)
+        K, V = layer.cache_views(li)
+        mi.gen_bf16_device(wl.seed, mi.stream_id(mi.KIND_KCACHE, li), K.numel(), wl.sigma_cache,
+                           K.data_ptr(), s)
+        mi.gen_bf16_device(wl.seed, mi.stream_id(mi.KIND_VCACHE, li), V.numel(), wl.sigma_cache,
+                           V.data_ptr(), s)
+    x = torch.from_numpy(wl.x().view(np.int16)).cuda()
+    y = torch.empty_like(x)
+    torch.cuda.synchronize()
+    pos0 = wl.pos0
+    for i in range(max(warmup, n_rot)):
+        layer.forward(i % n_rot, x, y, pos0)
+    torch.cuda.synchronize()
+    n = max(steps - steps % n_rot, n_rot)
+    t0 = time.perf_counter()
+    for i in range(n):
+        layer.forward(i % n_rot, x, y, pos0)
+    torch.cuda.synchronize()
+    ms = (time.perf_counter() - t0) * 1e3 / n
+
+    def step():
+        for li in range(n_rot):
+            layer.forward(li, x, y, pos0)
+
+    ms_graph = graph_ms(step, max(n // n_rot, 5), 2) / n_rot
+    moe.attn_profile_enable(layer.ctx, 8 * n + 8)
+    for i in range(n):
+        layer.forward(i % n_rot, x, y, pos0)
+    torch.cuda.synchronize()
+    prof, _ = moe.attn_profile_read(layer.ctx)
+    moe.attn_profile_enable(layer.ctx, 0)
+    kern = {k: v[0] / v[1] * 1e3 for k, v in prof.items() if v[1]}
+    wqkv_b, wo_b = wl.d * wl.nqkv * 2, wl.n_heads * wl.hd * wl.d * 2
+    kv_b = 2 * wl.n_kv * (pos0 + 1) * wl.hd * 2
+    step_b = wqkv_b + wo_b + wl.d * 4 + kv_b + 2 * wl.d * 2
+    qkv_b = wqkv_b + wl.d * 2
+    best = min(ms, ms_graph)
+    out = {"workload": "dbrx_attention_decode", "T": 1, "context": pos0 + 1,
+           "rotation_layers": n_rot, "us_per_layer": best * 1e3, "us_direct_launch": ms * 1e3,
+           "us_graph": ms_graph * 1e3, "hbm_bytes_per_step": step_b,
+           "hbm_gbs": step_b / (best * 1e-3) / 1e9,
+           "hbm_frac": step_b / (best * 1e-3) / 1e9 / HBM_PEAK_GBS, "kernels_us": kern,
+           "roofline": {"bound": "hbm", "kernel": "qkv", "achieved": qkv_b / (kern["qkv"] * 1e-6) / 1e9,
+                        "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                        "frac": qkv_b / (kern["qkv"] * 1e-6) / 1e9 / HBM_PEAK_GBS,
+                        "algorithmic_bytes": qkv_b}}
+    log(f"attention decode: {best * 1e3:.1f} us/layer ({out['hbm_gbs']:.0f} GB/s), kernels {kern}")
+    layer.close()
+    del layer, stg, stg2, x, y
+    return out
+
+
 def stream_read_gbs(nbytes=4 << 30, reps=20):
     """GB/s of the library's plain streaming read (moe_diag_stream_read) over
     a 4 GiB buffer, far past the 256 MB last-level cache: the achievable HBM
@@ -638,6 +718,9 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-ep-share", action="store_true")
     ap.add_argument("--no-stack", action="store_true")
+    ap.add_argument("--no-attn", action="store_true")
+    ap.add_argument("--attn-only", action="store_true",
+                    help="time only the attention block (for profiling)")
     ap.add_argument("--stack-steps", type=int, default=20)
     ap.add_argument("--prefill-only", action="store_true",
                     help="time only the prefill layer (for counter collection)")
@@ -686,6 +769,10 @@ def main():
         src, dst = pool_take(1 << 30), pool_take(1 << 30)
         dst.copy_(src)          # reads 1 GiB, writes 1 GiB
         pool_reset()
+    if args.attn_only:
+        print(json.dumps({"attention": attn_section(args.steps, args.warmup)}), flush=True)
+        pool_release()
+        return
     if args.prefill_only:
         pw = mi.WORKLOADS["prefill"]
         player, px = setup_layer(pw, max_tokens=pw.T)
@@ -764,6 +851,11 @@ def main():
         del player, px
         torch.cuda.empty_cache()
 
+    attention = None
+    if not args.no_attn:
+        log("timing the attention block (decode) ...")
+        attention = attn_section(args.steps, args.warmup)
+
     ep_share = None
     if not args.no_ep_share:
         log("timing the expert-parallel shares ...")
@@ -821,6 +913,7 @@ def main():
         "cpu_baseline": cpu,
         "prefill": prefill,
         "ep_share": ep_share,
+        "attention": attention,
         "stack": stack,
         "perf_model": model,
     }

@@ -38,7 +38,7 @@ extern "C" {
 typedef struct attn_ctx attn_ctx;
 
 /* Block configuration.
- *   d_model    : D_embed, a multiple of 256.
+ *   d_model    : D_embed, a multiple of 256, at most 8192.
  *   n_heads, n_kv_heads, head_dim : query heads, key/value heads (dividing
  *                n_heads) and their width, 64 or 128; (n_heads + 2
  *                n_kv_heads) head_dim is D_qkv_hidden, a multiple of 16, and
@@ -57,8 +57,11 @@ typedef struct {
 } attn_config;
 
 /* Bytes of the caller-allocated weight arena (per layer: gamma fp32 [d]
- * padded to 256 B, then Wqkv and Wo repacked into the fragment-tiled layout
- * of moe.h's experts), of the key/value cache, and of the workspace; 0 if
+ * padded to 256 B, the rotary frequencies fp64 [head_dim/2] padded to 256 B,
+ * then Wqkv and Wo repacked into the fragment-tiled layout
+ * of moe.h's experts, the query and key rows of Wqkv reordered within each
+ * head so that the two members of every rotation pair share a 16-row tile),
+ * of the key/value cache, and of the workspace; 0 if
  * cfg is invalid.  Cache layout, per layer l: K then V, each bf16
  * [n_kv_heads][max_seq][head_dim] (head-major, positions contiguous), so K of
  * layer l head g position p starts at element
@@ -106,13 +109,12 @@ MOE_API moe_status attn_intermediates(const attn_ctx *ctx, const uint16_t **h, c
  * kinds of attn_kernel_kind. */
 typedef enum {
     ATTN_K_NORM = 0,       /* layer norm */
-    ATTN_K_QKV = 1,        /* fused projection GEMV */
-    ATTN_K_ROPE = 2,       /* rotary encoding + cache append */
-    ATTN_K_SCORE = 3,      /* attention over position chunks */
-    ATTN_K_COMBINE = 4,    /* merge of the chunks */
-    ATTN_K_OUT = 5,        /* output projection GEMV + residual */
-    ATTN_K_PACK = 6,       /* weight repacking */
-    ATTN_K_COUNT = 7
+    ATTN_K_QKV = 1,        /* fused projection + rotary + cache append */
+    ATTN_K_SCORE = 2,      /* attention over position chunks */
+    ATTN_K_COMBINE = 3,    /* merge of the chunks */
+    ATTN_K_OUT = 4,        /* output projection + residual */
+    ATTN_K_PACK = 5,       /* weight repacking */
+    ATTN_K_COUNT = 6
 } attn_kernel_kind;
 MOE_API moe_status attn_profile_enable(attn_ctx *ctx, int32_t max_launches);
 MOE_API moe_status attn_profile_read(attn_ctx *ctx, double *total_ms, int64_t *launches,

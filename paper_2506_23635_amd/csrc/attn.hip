@@ -1,25 +1,26 @@
 // attn.hip -- kernels of the self-attention block of include/attn.h for a few
 // new tokens (T <= 16: decode), in launch order:
 //
-//   norm_kernel     layer norm of x, one workgroup per token (fp32 statistics,
-//                   fixed reduction order), h = bf16((x - mean) rstd gamma)
-//   gemv_kernel<kQkv>  q|k|v = h Wqkv, fp32
-//   rope_kernel     rotary encoding of the query and key heads (angles in
-//                   fp64, rotation in fp32), bf16 q to the workspace, bf16 k
-//                   and v appended to the cache
+//   norm_kernel     layer norm, one workgroup per token (one pass, fp64
+//                   sums, fixed reduction order), h = bf16((x - mean) rstd gamma)
+//   qkv_kernel      q|k|v = h Wqkv, and in its epilogue the rotary encoding
+//                   of the query and key heads (angles reduced in fp64,
+//                   rotation in fp32): bf16 q to the workspace, bf16 k and v
+//                   appended to the cache
 //   score_kernel    attention of every query head of one key/value head over
-//                   one chunk of 256 positions: scores, the chunk's softmax
-//                   maximum and sum, and the unnormalised weighted sum of v
+//                   one chunk of 64 positions (4 waves): scores on the matrix
+//                   cores, the chunk's softmax maximum and sum, and the
+//                   unnormalised weighted sum of v
 //   combine_kernel  merges the chunks of each (token, head) into bf16 a
-//   gemv_kernel<kOut>  o = a Wo (fp32) and y = bf16(x + o)
+//   gemv_kernel     o = a Wo (fp32) and y = bf16(x + o)
 //
 // The GEMVs stream the fragment-tiled weights (the layout of moe_common.h)
 // through v_mfma_f32_16x16x32_bf16 with the tokens as the B operand, as the
 // MoE decode GEMVs do: one workgroup per 16 output features, its 8 waves
 // splitting K (wave w takes K tiles w, w + 8, ...), wave 0 adding the
-// partial fragments in wave order.  The attention is VALU work: per token
-// and head it is q . k over hd for each position and a weighted sum of v,
-// small beside the projections' weight stream.
+// partial fragments in wave order.  In the attention, q . k of 16 positions
+// and 16 query rows is one MFMA per 32 dims; the weighted sum of v is VALU
+// work, small beside the projections' weight stream.
 #include "moe_common.h"
 
 namespace attn {
@@ -30,12 +31,9 @@ using moe::kTileK;
 using moe::kTileBytes;
 using moe::kTileRows;
 
-constexpr int kNormThreads = 256;
 constexpr int kSplit = 8;          // waves per GEMV workgroup (K split)
 constexpr int kUnroll = 8;         // K tiles per wave in flight
-constexpr int kChunk = 256;        // positions per attention workgroup (one per thread)
-constexpr int kRowBatch = 16;      // query rows whose P is held in LDS at once
-constexpr int kMaxRows = 16 * 8;   // tokens (16) x query heads per key/value head (8)
+constexpr int kChunk = 64;         // positions per attention workgroup
 constexpr int kPartPad = 4;        // m, l and padding after the hd sums of a partial
 
 __device__ inline u32x4_t ld16_nt(const void* p)
@@ -45,76 +43,17 @@ __device__ inline u32x4_t ld16_nt(const void* p)
 
 __device__ inline u32x4_t ld16(const void* p) { return *reinterpret_cast<const u32x4_t*>(p); }
 
-// sum over the 256 threads of a workgroup: lane butterfly, then the 4 wave
-// sums in wave order (the same order every time)
-__device__ inline float block_sum(float v, float* red)
-{
-    for (int off = 32; off >= 1; off >>= 1) v += __shfl_xor(v, off, 64);
-    const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
-    __syncthreads();
-    if (lane == 0) red[w] = v;
-    __syncthreads();
-    return ((red[0] + red[1]) + red[2]) + red[3];
-}
-
-__global__ __launch_bounds__(kNormThreads) void norm_kernel(const uint16_t* __restrict__ x,
-                                                            const float* __restrict__ gamma,
-                                                            int d, float eps,
-                                                            uint16_t* __restrict__ h)
-{
-    __shared__ float red[4];
-    const int t = blockIdx.x;
-    const uint16_t* xr = x + (int64_t)t * d;
-    // thread i holds the 8-element groups i, i + 256, ... (d % 256 == 0)
-    float s = 0.f;
-    for (int g = threadIdx.x; g < d / 8; g += kNormThreads) {
-        const u32x4_t v = ld16(xr + g * 8);
-#pragma unroll
-        for (int k = 0; k < 4; ++k)
-            s += __uint_as_float(v[k] << 16) + __uint_as_float(v[k] & 0xFFFF0000u);
-    }
-    const float mean = block_sum(s, red) / (float)d;
-    float q = 0.f;
-    for (int g = threadIdx.x; g < d / 8; g += kNormThreads) {
-        const u32x4_t v = ld16(xr + g * 8);
-#pragma unroll
-        for (int k = 0; k < 4; ++k) {
-            const float a = __uint_as_float(v[k] << 16) - mean;
-            const float b = __uint_as_float(v[k] & 0xFFFF0000u) - mean;
-            q = fmaf(a, a, q);
-            q = fmaf(b, b, q);
-        }
-    }
-    const float var = block_sum(q, red) / (float)d;
-    const float rstd = 1.0f / sqrtf(var + eps);
-    for (int g = threadIdx.x; g < d / 8; g += kNormThreads) {
-        const u32x4_t v = ld16(xr + g * 8);
-        const float4 g0 = *reinterpret_cast<const float4*>(gamma + g * 8);
-        const float4 g1 = *reinterpret_cast<const float4*>(gamma + g * 8 + 4);
-        const float gm[8] = {g0.x, g0.y, g0.z, g0.w, g1.x, g1.y, g1.z, g1.w};
-        u32x4_t out;
-#pragma unroll
-        for (int k = 0; k < 4; ++k) {
-            const float a = (__uint_as_float(v[k] << 16) - mean) * rstd * gm[2 * k];
-            const float b = (__uint_as_float(v[k] & 0xFFFF0000u) - mean) * rstd * gm[2 * k + 1];
-            out[k] = (uint32_t)moe::f32_to_bf16(a) | ((uint32_t)moe::f32_to_bf16(b) << 16);
-        }
-        *reinterpret_cast<u32x4_t*>(h + (int64_t)t * d + g * 8) = out;
-    }
-}
-
-enum { kQkv = 0, kOut = 1 };
-
+// The output projection, o = a Wo (fp32) and y = bf16(x + o), one
+// workgroup per 16 output features.
 struct GemvArgs {
     const uint8_t* w;      // packed weights: N/16 row tiles of K/32 tiles
     const uint16_t* x;     // [T][K] bf16
     float* y32;            // [T][N] fp32
-    const uint16_t* res;   // kOut: residual [T][N] bf16
-    uint16_t* y16;         // kOut: bf16(res + y) [T][N]
+    const uint16_t* res;   // residual [T][N] bf16
+    uint16_t* y16;         // bf16(res + y) [T][N]
     int K, N, T;
 };
 
-template <int kMode>
 __global__ __launch_bounds__(64 * kSplit) void gemv_kernel(GemvArgs a)
 {
     __shared__ f32x4_t s_red[(kSplit - 1) * 64];
@@ -152,61 +91,175 @@ __global__ __launch_bounds__(64 * kSplit) void gemv_kernel(GemvArgs a)
     // lane holds output features 16q + 4g .. +3 of token j
     const int64_t o = (int64_t)j * a.N + q * kTileRows + g * 4;
     *reinterpret_cast<float4*>(a.y32 + o) = make_float4(acc[0], acc[1], acc[2], acc[3]);
-    if (kMode == kOut) {
-        const uint2 r = *reinterpret_cast<const uint2*>(a.res + o);
-        const float r0 = __uint_as_float(r.x << 16), r1 = __uint_as_float(r.x & 0xFFFF0000u);
-        const float r2 = __uint_as_float(r.y << 16), r3 = __uint_as_float(r.y & 0xFFFF0000u);
-        const uint32_t lo = (uint32_t)moe::f32_to_bf16(r0 + acc[0]) |
-                            ((uint32_t)moe::f32_to_bf16(r1 + acc[1]) << 16);
-        const uint32_t hi = (uint32_t)moe::f32_to_bf16(r2 + acc[2]) |
-                            ((uint32_t)moe::f32_to_bf16(r3 + acc[3]) << 16);
-        *reinterpret_cast<uint2*>(a.y16 + o) = make_uint2(lo, hi);
+    const uint2 r = *reinterpret_cast<const uint2*>(a.res + o);
+    const float r0 = __uint_as_float(r.x << 16), r1 = __uint_as_float(r.x & 0xFFFF0000u);
+    const float r2 = __uint_as_float(r.y << 16), r3 = __uint_as_float(r.y & 0xFFFF0000u);
+    const uint32_t lo = (uint32_t)moe::f32_to_bf16(r0 + acc[0]) |
+                        ((uint32_t)moe::f32_to_bf16(r1 + acc[1]) << 16);
+    const uint32_t hi = (uint32_t)moe::f32_to_bf16(r2 + acc[2]) |
+                        ((uint32_t)moe::f32_to_bf16(r3 + acc[3]) << 16);
+    *reinterpret_cast<uint2*>(a.y16 + o) = make_uint2(lo, hi);
+}
+
+// Layer norm, one workgroup of 256 threads per token: the thread's 8-element
+// groups of x are loaded once into registers, x and x^2 summed in fp64 (so
+// E[x^2] - mean^2 loses nothing), a butterfly per wave and the 4 wave sums in
+// wave order, then h = bf16((x - mean) rstd gamma) from the registers.
+constexpr int kNormThreads = 256;
+constexpr int kNormGroups = 4;     // 8-element groups per thread (d <= 8192)
+
+__global__ __launch_bounds__(kNormThreads) void norm_kernel(const uint16_t* __restrict__ x,
+                                                            const float* __restrict__ gamma,
+                                                            int d, float eps,
+                                                            uint16_t* __restrict__ h)
+{
+    __shared__ double red[2][kNormThreads / 64];
+    const int t = blockIdx.x;
+    const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+    const uint16_t* xr = x + (int64_t)t * d;
+    u32x4_t v[kNormGroups];
+    double sx = 0.0, sq = 0.0;
+#pragma unroll
+    for (int k = 0; k < kNormGroups; ++k) {
+        const int e = threadIdx.x + k * kNormThreads;
+        const u32x4_t zero = {0u, 0u, 0u, 0u};
+        v[k] = e < d / 8 ? ld16(xr + e * 8) : zero;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            const double lo = __uint_as_float(v[k][i] << 16);
+            const double hi = __uint_as_float(v[k][i] & 0xFFFF0000u);
+            sx += lo + hi;
+            sq = fma(lo, lo, fma(hi, hi, sq));
+        }
+    }
+    for (int off = 32; off >= 1; off >>= 1) {
+        sx += __shfl_xor(sx, off, 64);
+        sq += __shfl_xor(sq, off, 64);
+    }
+    if (lane == 0) { red[0][w] = sx; red[1][w] = sq; }
+    __syncthreads();
+    const double m1 = ((red[0][0] + red[0][1]) + red[0][2]) + red[0][3];
+    const double m2 = ((red[1][0] + red[1][1]) + red[1][2]) + red[1][3];
+    const double mean = m1 / d;
+    const float rstd = (float)(1.0 / sqrt(fmax(m2 / d - mean * mean, 0.0) + (double)eps));
+    const float mu = (float)mean;
+#pragma unroll
+    for (int k = 0; k < kNormGroups; ++k) {
+        const int e = threadIdx.x + k * kNormThreads;
+        if (e >= d / 8) break;
+        const float4 g0 = *reinterpret_cast<const float4*>(gamma + e * 8);
+        const float4 g1 = *reinterpret_cast<const float4*>(gamma + e * 8 + 4);
+        const float gm[8] = {g0.x, g0.y, g0.z, g0.w, g1.x, g1.y, g1.z, g1.w};
+        u32x4_t out;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            const float lo = (__uint_as_float(v[k][i] << 16) - mu) * rstd * gm[2 * i];
+            const float hi = (__uint_as_float(v[k][i] & 0xFFFF0000u) - mu) * rstd * gm[2 * i + 1];
+            out[i] = (uint32_t)moe::f32_to_bf16(lo) | ((uint32_t)moe::f32_to_bf16(hi) << 16);
+        }
+        *reinterpret_cast<u32x4_t*>(h + (int64_t)t * d + e * 8) = out;
     }
 }
 
-struct RopeArgs {
-    const float* qkv;      // [T][nqkv]: query heads, key heads, value heads
+// The fused projection q|k|v = h Wqkv, one workgroup per 16 packed rows (8
+// waves splitting K, as gemv_kernel).  The query and key heads are packed
+// with rope_row, so in the epilogue lane (token j, group g), which holds
+// rows 4g..4g+3 of the tile, and lane l ^ 32 hold the two members of four
+// rotation pairs: the rotation (angle formed and reduced in fp64 from the
+// layer's frequency table, sincosf, product in fp32) and the bf16 rounding
+// happen there, q goes to the workspace and k, v to the cache at position
+// pos0 + j; the unrotated fp32 values are kept for inspection.
+struct QkvArgs {
+    const uint8_t* w;      // packed Wqkv, query and key heads permuted by rope_row
+    const uint16_t* h;     // [T][d] bf16, the normalised input
+    const double* inv_freq;  // [hd/2]: theta^(-2f/hd)
+    float* qkv;            // [T][nqkv] fp32, natural order, before rotation
     uint16_t* q;           // [T][H][hd]
     uint16_t* kc;          // this layer's K cache [G][max_seq][hd]
     uint16_t* vc;          // this layer's V cache
-    int T, H, G, hd, max_seq, pos0;
-    double log_theta;
+    int d, T, H, G, hd, max_seq, pos0;
 };
 
-// one thread per (token, head slot, pair i): slot s < H is query head s,
-// H <= s < H + G key head s - H, then value heads (no rotation)
-__global__ __launch_bounds__(256) void rope_kernel(RopeArgs a)
+// cos and sin of pos * inv_freq: the angle is formed and reduced modulo 2 pi
+// in fp64 (2 pi split in two parts, Cody and Waite), so sincosf only sees an
+// argument within [-pi, pi]
+__device__ inline void rope_cs(int pos, double inv_freq, float& c, float& s)
 {
-    const int half = a.hd / 2, slots = a.H + 2 * a.G;
-    const int64_t idx = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-    if (idx >= (int64_t)a.T * slots * half) return;
-    const int i = (int)(idx % half);
-    const int s = (int)((idx / half) % slots);
-    const int t = (int)(idx / ((int64_t)half * slots));
-    const int nqkv = slots * a.hd;
-    const float* src = a.qkv + (int64_t)t * nqkv + (int64_t)s * a.hd;
-    const int pos = a.pos0 + t;
-    const float x0 = src[i], x1 = src[i + half];
-    uint16_t* dst;
-    if (s >= a.H + a.G) {
-        dst = a.vc + ((int64_t)(s - a.H - a.G) * a.max_seq + pos) * a.hd;
-        dst[i] = moe::f32_to_bf16(x0);
-        dst[i + half] = moe::f32_to_bf16(x1);
-        return;
+    constexpr double kTwoPiHi = 6.28318530717958623200e+00;   // 2 pi rounded to fp64
+    constexpr double kTwoPiLo = 2.44929359829470635445e-16;   // 2 pi - kTwoPiHi
+    constexpr double kInvTwoPi = 1.59154943091895335769e-01;
+    const double ang = (double)pos * inv_freq;
+    const double k = rint(ang * kInvTwoPi);
+    const double r = fma(-k, kTwoPiLo, fma(-k, kTwoPiHi, ang));
+    sincosf((float)r, &s, &c);
+}
+
+__global__ __launch_bounds__(64 * kSplit) void qkv_kernel(QkvArgs a)
+{
+    __shared__ f32x4_t s_red[(kSplit - 1) * 64];
+    const int q = blockIdx.x;
+    const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+    const int j = lane & 15, g = lane >> 4;
+    const int KT = a.d / kTileK;
+    const uint8_t* pw = a.w + moe::tile_offset(q, 0, KT) + lane * 16;
+    const bool has_tok = j < a.T;
+    const uint16_t* px = a.h + (has_tok ? (int64_t)j * a.d : 0) + g * 8;
+    f32x4_t acc = {0.f, 0.f, 0.f, 0.f};
+    const u32x4_t zero = {0u, 0u, 0u, 0u};
+    int kt = 0;
+    for (; kt + kSplit * kUnroll <= KT; kt += kSplit * kUnroll) {
+        u32x4_t wv[kUnroll], xb[kUnroll];
+#pragma unroll
+        for (int u = 0; u < kUnroll; ++u)
+            wv[u] = ld16_nt(pw + (int64_t)(kt + w + kSplit * u) * kTileBytes);
+#pragma unroll
+        for (int u = 0; u < kUnroll; ++u)
+            xb[u] = has_tok ? ld16(px + (kt + w + kSplit * u) * kTileK) : zero;
+#pragma unroll
+        for (int u = 0; u < kUnroll; ++u) acc = moe::mfma16x16x32(wv[u], xb[u], acc);
     }
-    // angle pos * theta^(-2i/hd), in fp64
-    const double ang = (double)pos * exp(-(2.0 * i / a.hd) * a.log_theta);
-    double sn, cs;
-    sincos(ang, &sn, &cs);
-    const float c = (float)cs, sf = (float)sn;
-    const float r0 = x0 * c - x1 * sf;
-    const float r1 = x1 * c + x0 * sf;
-    if (s < a.H)
-        dst = a.q + ((int64_t)t * a.H + s) * a.hd;
-    else
-        dst = a.kc + ((int64_t)(s - a.H) * a.max_seq + pos) * a.hd;
-    dst[i] = moe::f32_to_bf16(r0);
-    dst[i + half] = moe::f32_to_bf16(r1);
+    for (kt += w; kt < KT; kt += kSplit) {
+        const u32x4_t wv = ld16_nt(pw + (int64_t)kt * kTileBytes);
+        const u32x4_t xb = has_tok ? ld16(px + kt * kTileK) : zero;
+        acc = moe::mfma16x16x32(wv, xb, acc);
+    }
+    if (w > 0) s_red[(w - 1) * 64 + lane] = acc;
+    __syncthreads();
+    if (w != 0) return;
+    for (int i = 0; i + 1 < kSplit; ++i) acc += s_red[i * 64 + lane];
+    if (!has_tok) return;
+    const int hd = a.hd, half = hd / 2;
+    const int nqk = (a.H + a.G) * hd, nqkv = nqk + a.G * hd;
+    const int row0 = q * kTileRows;
+    const int pos = a.pos0 + j;
+    float* qrow = a.qkv + (int64_t)j * nqkv;
+    uint16_t* dst;
+    float r[4];
+    if (row0 < nqk) {
+        const int head = row0 / hd, m = (row0 % hd) / kTileRows;
+        const bool second = g >= 2;
+        const int f0 = 8 * m + 4 * (g & 1);           // frequency index of acc[0]
+        const int i0 = (second ? half : 0) + f0;       // feature index in the head
+        *reinterpret_cast<float4*>(qrow + head * hd + i0) = make_float4(acc[0], acc[1], acc[2], acc[3]);
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+            const float partner = __shfl_xor(acc[e], 32, 64);
+            float c, sf;
+            rope_cs(pos, a.inv_freq[f0 + e], c, sf);
+            r[e] = second ? acc[e] * c + partner * sf : acc[e] * c - partner * sf;
+        }
+        dst = head < a.H ? a.q + ((int64_t)j * a.H + head) * hd + i0
+                         : a.kc + ((int64_t)(head - a.H) * a.max_seq + pos) * hd + i0;
+    } else {
+        const int n = row0 + 4 * g;                    // value features: natural order
+        *reinterpret_cast<float4*>(qrow + n) = make_float4(acc[0], acc[1], acc[2], acc[3]);
+#pragma unroll
+        for (int e = 0; e < 4; ++e) r[e] = acc[e];
+        dst = a.vc + ((int64_t)((n - nqk) / hd) * a.max_seq + pos) * hd + (n - nqk) % hd;
+    }
+    const uint32_t lo = (uint32_t)moe::f32_to_bf16(r[0]) | ((uint32_t)moe::f32_to_bf16(r[1]) << 16);
+    const uint32_t hi = (uint32_t)moe::f32_to_bf16(r[2]) | ((uint32_t)moe::f32_to_bf16(r[3]) << 16);
+    *reinterpret_cast<uint2*>(dst) = make_uint2(lo, hi);
 }
 
 struct ScoreArgs {
@@ -218,108 +271,151 @@ struct ScoreArgs {
     float scale;           // 1 / sqrt(hd)
 };
 
-// Workgroup (key/value head g, chunk c): thread p owns position
-// c * 256 + p.  The query rows are every (token t, query head j of g); row
-// r's positions end at pos0 + t (causal).  Per batch of 16 rows: scores in
-// fp32 (q . k in index order, times the scale), the chunk's maximum and the
-// sum of exp(s - max) per row (fixed-order reductions), P in LDS, then
-// thread (row, 8 or 4 dims) sums P v over the chunk's positions in order.
+// One workgroup of 4 waves per (key/value head g, chunk c of 64 positions);
+// wave w owns positions 16 w .. 16 w + 15 of the chunk.  The query rows are
+// every (token t, query head j of g), r = t * group + jj, in batches of 16;
+// row r sees positions up to pos0 + t (causal).
+//
+// Scores on the matrix cores: v_mfma_f32_16x16x32_bf16 with the wave's 16
+// positions x 32 dims of K as the A operand (lane l: position l%16, dims
+// 8(l/16)..+7) and the batch's q rows as B, so lane l ends with the scores of
+// query row l%16 at positions 16 w + 4(l/16) + i (i = 0..3).  The chunk's
+// maximum per row is the maximum of the four waves' (two butterfly steps in
+// the wave, then LDS), exp(s - max) goes to LDS and the chunk's sum adds the
+// waves' sums in wave order.  Then wave w sums P v over all 64 positions for
+// dims w hd/4 .. (w+1) hd/4 - 1: lane l takes dims D(l%16)..+D-1 of that
+// quarter at positions 4k + l/16 (V staged in LDS, rows padded so the four
+// position groups hit distinct banks), two butterfly steps adding the four
+// position groups in a fixed order.
 template <int HD>
-__global__ __launch_bounds__(kChunk) void score_kernel(ScoreArgs a)
+__global__ __launch_bounds__(256) void score_kernel(ScoreArgs a)
 {
-    __shared__ uint16_t qs[kMaxRows][HD];                 // query rows (bf16)
-    __shared__ uint16_t vs[kChunk][HD];                   // the chunk's values
-    __shared__ float ps[kRowBatch][kChunk];               // exp(s - max) of a batch
-    __shared__ float red[4][kRowBatch];
+    constexpr int kPos = 64;           // positions per workgroup
+    constexpr int kWaves = 4;          // 16 positions per wave
+    constexpr int KS = HD / 32;        // MFMA K steps over the head
+    constexpr int DQ = HD / kWaves;    // dims per wave in P v
+    constexpr int D = DQ / 16;         // dims per lane in P v
+    constexpr int VROW = HD + 32;      // padded V row (bf16)
+    __shared__ __attribute__((aligned(16))) uint16_t vs[kPos * VROW];
+    __shared__ float ps[16][kPos + 4];
+    __shared__ float mx[kWaves][16], lx[kWaves][16];
     const int g = blockIdx.x, c = blockIdx.y;
     const int group = a.H / a.G;
     const int R = a.T * group;
-    const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
-    const int pos = c * kChunk + tid;
+    const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+    const int p0 = c * kPos;
     const int n_pos = a.pos0 + a.T;
-    // query rows r = t * group + jj -> head j = g * group + jj
-    for (int e = tid; e < R * HD / 8; e += kChunk) {
-        const int r = e / (HD / 8), k8 = e % (HD / 8);
-        const int t = r / group, j = g * group + r % group;
-        *reinterpret_cast<u32x4_t*>(&qs[r][k8 * 8]) =
-            ld16(a.q + ((int64_t)t * a.H + j) * HD + k8 * 8);
+    const int last = min(kPos, n_pos - p0);          // live positions of the chunk
+    const uint16_t* kbase = a.kc + (int64_t)g * a.max_seq * HD;
+    const uint16_t* vbase = a.vc + (int64_t)g * a.max_seq * HD;
+    const u32x4_t zero = {0u, 0u, 0u, 0u};
+    // K fragments of the wave's 16 positions (A operands), loaded once
+    u32x4_t kf[KS];
+    {
+        const int p = w * 16 + (lane & 15);
+#pragma unroll
+        for (int ks = 0; ks < KS; ++ks)
+            kf[ks] = p < last ? ld16(kbase + (int64_t)(p0 + p) * HD + ks * 32 + (lane >> 4) * 8)
+                              : zero;
     }
-    u32x4_t kreg[HD / 8];
-    const bool live = pos < n_pos;
-    const uint16_t* kp = a.kc + ((int64_t)g * a.max_seq + (live ? pos : 0)) * HD;
-    const uint16_t* vp = a.vc + ((int64_t)g * a.max_seq + (live ? pos : 0)) * HD;
-#pragma unroll
-    for (int k8 = 0; k8 < HD / 8; ++k8) {
-        const u32x4_t zero = {0u, 0u, 0u, 0u};
-        kreg[k8] = live ? ld16(kp + k8 * 8) : zero;
-        *reinterpret_cast<u32x4_t*>(&vs[tid][k8 * 8]) = live ? ld16(vp + k8 * 8) : zero;
+    // V of the wave's 16 positions into LDS (16-byte pieces, coalesced)
+    for (int e = lane; e < 16 * (HD / 8); e += 64) {
+        const int p = w * 16 + e / (HD / 8), k8 = e % (HD / 8);
+        *reinterpret_cast<u32x4_t*>(&vs[p * VROW + k8 * 8]) =
+            p < last ? ld16(vbase + (int64_t)(p0 + p) * HD + k8 * 8) : zero;
     }
-    __syncthreads();
-    for (int b0 = 0; b0 < R; b0 += kRowBatch) {
-        float s[kRowBatch];
+    const int dg = lane & 15, pq = lane >> 4;
+    for (int b0 = 0; b0 < R; b0 += 16) {
+        const int c_row = b0 + dg;                      // this lane's query row
+        const bool row_ok = c_row < R;
+        const int t_row = row_ok ? c_row / group : 0;
+        const int j_row = g * group + (row_ok ? c_row % group : 0);
+        const uint16_t* qrow = a.q + ((int64_t)t_row * a.H + j_row) * HD + pq * 8;
+        f32x4_t acc = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-        for (int rr = 0; rr < kRowBatch; ++rr) {
-            const int r = b0 + rr;
-            float acc = 0.f;
-            if (r < R) {
+        for (int ks = 0; ks < KS; ++ks) {
+            const u32x4_t qb = row_ok ? ld16(qrow + ks * 32) : zero;
+            acc = moe::mfma16x16x32(kf[ks], qb, acc);
+        }
+        // scale, causal mask, the chunk's maximum per row
+        const int lim = a.pos0 + t_row;
+        float sv[4];
+        float m = -INFINITY;
 #pragma unroll
-                for (int k8 = 0; k8 < HD / 8; ++k8) {
-                    const u32x4_t qv = *reinterpret_cast<const u32x4_t*>(&qs[r][k8 * 8]);
+        for (int i = 0; i < 4; ++i) {
+            const int pos = p0 + w * 16 + pq * 4 + i;
+            sv[i] = (row_ok && pos <= lim) ? acc[i] * a.scale : -INFINITY;
+            m = fmaxf(m, sv[i]);
+        }
+        m = fmaxf(m, __shfl_xor(m, 16, 64));
+        m = fmaxf(m, __shfl_xor(m, 32, 64));
+        if (lane < 16) mx[w][lane] = m;
+        __syncthreads();
+        m = fmaxf(fmaxf(mx[0][dg], mx[1][dg]), fmaxf(mx[2][dg], mx[3][dg]));
+        float l = 0.f;
 #pragma unroll
-                    for (int e = 0; e < 4; ++e) {
-                        acc = fmaf(__uint_as_float(qv[e] << 16), __uint_as_float(kreg[k8][e] << 16), acc);
-                        acc = fmaf(__uint_as_float(qv[e] & 0xFFFF0000u),
-                                   __uint_as_float(kreg[k8][e] & 0xFFFF0000u), acc);
-                    }
+        for (int i = 0; i < 4; ++i) {
+            const float p = sv[i] == -INFINITY ? 0.f : expf(sv[i] - m);
+            l += p;
+            ps[dg][w * 16 + pq * 4 + i] = p;
+        }
+        l += __shfl_xor(l, 16, 64);
+        l += __shfl_xor(l, 32, 64);
+        if (lane < 16) lx[w][lane] = l;
+        __syncthreads();
+        // row statistics of the chunk: wave 0, lanes of the first position group
+        if (w == 0 && pq == 0 && row_ok) {
+            float* out = a.part + (((int64_t)t_row * a.H + j_row) * a.n_chunks + c) * (HD + kPartPad);
+            out[HD] = m;
+            out[HD + 1] = ((lx[0][dg] + lx[1][dg]) + lx[2][dg]) + lx[3][dg];
+        }
+        // P v for this wave's quarter of the dims, 8 rows at a time
+        const int nb = min(16, R - b0);
+        for (int r0 = 0; r0 < nb; r0 += 8) {
+            float o[8][D];
+#pragma unroll
+            for (int rr = 0; rr < 8; ++rr)
+#pragma unroll
+                for (int e = 0; e < D; ++e) o[rr][e] = 0.f;
+#pragma unroll 4
+            for (int k = 0; k < kPos / 4; ++k) {
+                const int p = 4 * k + pq;
+                const uint16_t* vr = &vs[p * VROW + w * DQ + dg * D];
+                float vv[D];
+                if constexpr (D == 2) {
+                    const uint32_t w2 = *reinterpret_cast<const uint32_t*>(vr);
+                    vv[0] = __uint_as_float(w2 << 16);
+                    vv[1] = __uint_as_float(w2 & 0xFFFF0000u);
+                } else {
+                    vv[0] = __uint_as_float((uint32_t)vr[0] << 16);
+                }
+#pragma unroll
+                for (int rr = 0; rr < 8; ++rr) {
+                    const float pw = ps[r0 + rr][p];
+#pragma unroll
+                    for (int e = 0; e < D; ++e) o[rr][e] = fmaf(pw, vv[e], o[rr][e]);
                 }
             }
-            const bool ok = r < R && pos <= a.pos0 + r / group;
-            s[rr] = ok ? acc * a.scale : -INFINITY;
-        }
-        // per row: the chunk maximum over the 256 positions
-        float m[kRowBatch];
 #pragma unroll
-        for (int rr = 0; rr < kRowBatch; ++rr) {
-            float v = s[rr];
-            for (int off = 32; off >= 1; off >>= 1) v = fmaxf(v, __shfl_xor(v, off, 64));
-            if (lane == 0) red[w][rr] = v;
-        }
-        __syncthreads();
+            for (int rr = 0; rr < 8; ++rr)
 #pragma unroll
-        for (int rr = 0; rr < kRowBatch; ++rr)
-            m[rr] = fmaxf(fmaxf(red[0][rr], red[1][rr]), fmaxf(red[2][rr], red[3][rr]));
-        __syncthreads();
+                for (int e = 0; e < D; ++e) {
+                    float v = o[rr][e];
+                    v += __shfl_xor(v, 16, 64);
+                    v += __shfl_xor(v, 32, 64);
+                    o[rr][e] = v;
+                }
+            if (pq == 0) {
 #pragma unroll
-        for (int rr = 0; rr < kRowBatch; ++rr) {
-            const float p = s[rr] == -INFINITY ? 0.f : expf(s[rr] - m[rr]);
-            ps[rr][tid] = p;
-            float v = p;
-            for (int off = 32; off >= 1; off >>= 1) v += __shfl_xor(v, off, 64);
-            if (lane == 0) red[w][rr] = v;
-        }
-        __syncthreads();
-        // thread (row rr, dims dg * D .. +D-1), D = HD / 16
-        constexpr int D = HD / 16;
-        const int rr = tid / 16, dg = tid % 16;
-        const int r = b0 + rr;
-        if (r < R) {
-            float acc[D];
+                for (int rr = 0; rr < 8; ++rr) {
+                    const int r = b0 + r0 + rr;
+                    if (r < R) {
+                        const int t = r / group, j = g * group + r % group;
+                        float* out = a.part + (((int64_t)t * a.H + j) * a.n_chunks + c) * (HD + kPartPad);
 #pragma unroll
-            for (int e = 0; e < D; ++e) acc[e] = 0.f;
-            const int last = min(kChunk, n_pos - c * kChunk);
-            for (int p = 0; p < last; ++p) {
-                const float pv = ps[rr][p];
-#pragma unroll
-                for (int e = 0; e < D; ++e)
-                    acc[e] = fmaf(pv, __uint_as_float((uint32_t)vs[p][dg * D + e] << 16), acc[e]);
-            }
-            const int t = r / group, j = g * group + r % group;
-            float* out = a.part + (((int64_t)t * a.H + j) * a.n_chunks + c) * (HD + kPartPad);
-#pragma unroll
-            for (int e = 0; e < D; ++e) out[dg * D + e] = acc[e];
-            if (dg == 0) {
-                out[HD] = m[rr];
-                out[HD + 1] = ((red[0][rr] + red[1][rr]) + red[2][rr]) + red[3][rr];
+                        for (int e = 0; e < D; ++e) out[w * DQ + dg * D + e] = o[rr][e];
+                    }
+                }
             }
         }
         __syncthreads();
@@ -340,12 +436,15 @@ __global__ __launch_bounds__(128) void combine_kernel(CombineArgs a)
     const int i = threadIdx.x;
     if (i >= a.hd) return;
     const int used = (a.pos0 + t) / kChunk + 1;
-    const float* base = a.part + (int64_t)th * a.n_chunks * (a.hd + kPartPad);
+    const int stride = a.hd + kPartPad;
+    const float* base = a.part + (int64_t)th * a.n_chunks * stride;
     float M = -INFINITY;
-    for (int c = 0; c < used; ++c) M = fmaxf(M, base[(int64_t)c * (a.hd + kPartPad) + a.hd]);
+#pragma unroll 8
+    for (int c = 0; c < used; ++c) M = fmaxf(M, base[(int64_t)c * stride + a.hd]);
     float L = 0.f, acc = 0.f;
+#pragma unroll 8
     for (int c = 0; c < used; ++c) {
-        const float* pc = base + (int64_t)c * (a.hd + kPartPad);
+        const float* pc = base + (int64_t)c * stride;
         const float f = expf(pc[a.hd] - M);
         L = fmaf(pc[a.hd + 1], f, L);
         acc = fmaf(pc[i], f, acc);
@@ -365,45 +464,46 @@ hipError_t attn_launch_norm(const uint16_t* x, const float* gamma, int T, int d,
     return hipGetLastError();
 }
 
-hipError_t attn_launch_gemv(int out_mode, const void* w, const uint16_t* x, int T, int K, int N,
-                            float* y32, const uint16_t* res, uint16_t* y16, hipStream_t s)
+hipError_t attn_launch_qkv(const void* w, const uint16_t* h, const double* inv_freq, float* qkv,
+                           uint16_t* q, uint16_t* kc, uint16_t* vc, int T, int d, int H, int G,
+                           int hd, int max_seq, int pos0, hipStream_t s)
 {
-    attn::GemvArgs a{static_cast<const uint8_t*>(w), x, y32, res, y16, K, N, T};
-    if (out_mode)
-        hipLaunchKernelGGL(attn::gemv_kernel<attn::kOut>, dim3(N / moe::kTileRows),
-                           dim3(64 * attn::kSplit), 0, s, a);
-    else
-        hipLaunchKernelGGL(attn::gemv_kernel<attn::kQkv>, dim3(N / moe::kTileRows),
-                           dim3(64 * attn::kSplit), 0, s, a);
+    attn::QkvArgs a{static_cast<const uint8_t*>(w), h, inv_freq, qkv, q, kc, vc,
+                    d, T, H, G, hd, max_seq, pos0};
+    const int rows = (H + 2 * G) * hd;
+    hipLaunchKernelGGL(attn::qkv_kernel, dim3(rows / moe::kTileRows), dim3(64 * attn::kSplit), 0, s,
+                       a);
     return hipGetLastError();
 }
 
-hipError_t attn_launch_rope(const float* qkv, uint16_t* q, uint16_t* kc, uint16_t* vc, int T,
-                            int H, int G, int hd, int max_seq, int pos0, double theta,
-                            hipStream_t s)
+hipError_t attn_launch_out(const void* w, const uint16_t* x, int T, int K, int N, float* y32,
+                           const uint16_t* res, uint16_t* y16, hipStream_t s)
 {
-    attn::RopeArgs a{qkv, q, kc, vc, T, H, G, hd, max_seq, pos0, log(theta)};
-    const int64_t n = (int64_t)T * (H + 2 * G) * (hd / 2);
-    hipLaunchKernelGGL(attn::rope_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s, a);
+    attn::GemvArgs a{static_cast<const uint8_t*>(w), x, y32, res, y16, K, N, T};
+    hipLaunchKernelGGL(attn::gemv_kernel, dim3(N / moe::kTileRows), dim3(64 * attn::kSplit), 0, s, a);
     return hipGetLastError();
 }
 
 int attn_chunks(int n_pos) { return (n_pos + attn::kChunk - 1) / attn::kChunk; }
 int attn_part_stride(int hd) { return hd + attn::kPartPad; }
 
-hipError_t attn_launch_attention(const uint16_t* q, const uint16_t* kc, const uint16_t* vc,
-                                 float* part, uint16_t* out, int T, int H, int G, int hd,
-                                 int max_seq, int pos0, int n_chunks_alloc, hipStream_t s)
+hipError_t attn_launch_score(const uint16_t* q, const uint16_t* kc, const uint16_t* vc,
+                             float* part, int T, int H, int G, int hd, int max_seq, int pos0,
+                             int n_chunks_alloc, hipStream_t s)
 {
     const int n_chunks = attn_chunks(pos0 + T);
     attn::ScoreArgs a{q, kc, vc, part, T, H, G, max_seq, pos0, n_chunks_alloc,
                       (float)(1.0 / sqrt((double)hd))};
     if (hd == 128)
-        hipLaunchKernelGGL(attn::score_kernel<128>, dim3(G, n_chunks), dim3(attn::kChunk), 0, s, a);
+        hipLaunchKernelGGL(attn::score_kernel<128>, dim3(G, n_chunks), dim3(256), 0, s, a);
     else
-        hipLaunchKernelGGL(attn::score_kernel<64>, dim3(G, n_chunks), dim3(attn::kChunk), 0, s, a);
-    hipError_t e = hipGetLastError();
-    if (e != hipSuccess) return e;
+        hipLaunchKernelGGL(attn::score_kernel<64>, dim3(G, n_chunks), dim3(256), 0, s, a);
+    return hipGetLastError();
+}
+
+hipError_t attn_launch_combine(const float* part, uint16_t* out, int T, int H, int hd, int pos0,
+                               int n_chunks_alloc, hipStream_t s)
+{
     attn::CombineArgs c{part, out, H, hd, pos0, n_chunks_alloc};
     hipLaunchKernelGGL(attn::combine_kernel, dim3(T * H), dim3(128), 0, s, c);
     return hipGetLastError();

@@ -1,7 +1,8 @@
 // attn_capi.cpp -- the C-ABI of include/attn.h: configuration checks, the
 // carve-up of the caller's weight arena, cache and workspace, the one-time
-// weight repack, and the launch sequence of the block (norm -> fused
-// projection -> rotary + cache append -> attention over position chunks ->
+// weight repack (the query and key heads of Wqkv with their rotation pairs
+// in one tile), and the launch sequence of the block (norm -> fused
+// projection + rotary + cache append -> attention over position chunks ->
 // merge -> output projection + residual).  Nothing here allocates device
 // memory.
 #include <hip/hip_runtime.h>
@@ -25,7 +26,7 @@ constexpr int kMaxGroup = 8;       // query heads per key/value head (attention 
 size_t align_up(size_t v, size_t a) { return (v + a - 1) / a * a; }
 
 struct Layout {
-    size_t gamma_bytes, wqkv_off, wqkv_bytes, wo_off, wo_bytes, layer_bytes, arena_bytes;
+    size_t gamma_bytes, freq_off, wqkv_off, wqkv_bytes, wo_off, wo_bytes, layer_bytes, arena_bytes;
     size_t cache_head_elems, cache_layer_bytes, cache_bytes;
     size_t h_off, qkv_off, q_off, part_off, a_off, o_off, ws_bytes;
     int nqkv, nq, n_chunks;
@@ -34,7 +35,8 @@ struct Layout {
 const char* check_config(const attn_config* c)
 {
     if (!c) return "config is NULL";
-    if (c->d_model <= 0 || c->d_model % 256) return "d_model must be a positive multiple of 256";
+    if (c->d_model <= 0 || c->d_model % 256 || c->d_model > 8192)
+        return "d_model must be a multiple of 256 in [256, 8192]";
     if (c->head_dim != 64 && c->head_dim != 128) return "head_dim must be 64 or 128";
     if (c->n_heads < 1 || c->n_kv_heads < 1 || c->n_heads % c->n_kv_heads)
         return "n_kv_heads must divide n_heads";
@@ -59,7 +61,8 @@ Layout make_layout(const attn_config* c)
     L.nq = (int)(H * hd);
     L.nqkv = (int)((H + 2 * G) * hd);
     L.gamma_bytes = align_up(d * 4, kAlign);
-    L.wqkv_off = L.gamma_bytes;
+    L.freq_off = L.gamma_bytes;
+    L.wqkv_off = L.freq_off + align_up(hd / 2 * 8, kAlign);
     L.wqkv_bytes = d * L.nqkv * 2;
     L.wo_off = L.wqkv_off + align_up(L.wqkv_bytes, kAlign);
     L.wo_bytes = (size_t)L.nq * d * 2;
@@ -198,14 +201,23 @@ moe_status attn_load_layer(attn_ctx* ctx, int32_t layer, const float* gamma, con
     hipStream_t s = static_cast<hipStream_t>(stream);
     uint8_t* base = layer_w(ctx, layer);
     const int d = c.d_model;
+    // the rotary frequencies theta^(-2f/hd), once per layer beside gamma
+    std::vector<double> freq(c.head_dim / 2);
+    for (int f = 0; f < c.head_dim / 2; ++f)
+        freq[f] = std::pow((double)c.rope_theta, -2.0 * f / c.head_dim);
     hipError_t e;
     if (src_on_device) {
         if (misaligned(gamma) || misaligned(wqkv) || misaligned(wo))
             return fail(ctx, MOE_E_ALIGN, "device weight pointers must be 16-byte aligned");
         e = hipMemcpyAsync(base, gamma, (size_t)d * 4, hipMemcpyDeviceToDevice, s);
         if (e == hipSuccess)
+            e = hipMemcpyAsync(base + L.freq_off, freq.data(), freq.size() * 8,
+                               hipMemcpyHostToDevice, s);
+        if (e == hipSuccess) e = hipStreamSynchronize(s);   // freq is a host temporary
+        if (e == hipSuccess)
             e = timed(ctx, ATTN_K_PACK, s, [&] {
-                return moe_launch_pack(wqkv, d, L.nqkv, base + L.wqkv_off, 1, 0, s);
+                return moe_launch_pack_perm(wqkv, d, L.nqkv, base + L.wqkv_off, 1, 0, c.head_dim,
+                                            (c.n_heads + c.n_kv_heads) * c.head_dim, s);
             });
         if (e == hipSuccess)
             e = timed(ctx, ATTN_K_PACK, s, [&] {
@@ -220,7 +232,9 @@ moe_status attn_load_layer(attn_ctx* ctx, int32_t layer, const float* gamma, con
             return fail(ctx, MOE_E_ARG, "out of host memory for the host repack");
         }
         std::memcpy(tmp.data(), gamma, (size_t)d * 4);
-        moe_pack_host(wqkv, d, L.nqkv, tmp.data() + L.wqkv_off, 1, 0);
+        std::memcpy(tmp.data() + L.freq_off, freq.data(), freq.size() * 8);
+        moe_pack_host_perm(wqkv, d, L.nqkv, tmp.data() + L.wqkv_off, 1, 0, c.head_dim,
+                           (c.n_heads + c.n_kv_heads) * c.head_dim);
         moe_pack_host(wo, L.nq, d, tmp.data() + L.wo_off, 1, 0);
         e = hipMemcpyAsync(base, tmp.data(), tmp.size(), hipMemcpyHostToDevice, s);
         if (e == hipSuccess) e = hipStreamSynchronize(s);
@@ -258,22 +272,22 @@ moe_status attn_forward(attn_ctx* ctx, int32_t layer, const uint16_t* x, uint16_
     });
     if (e != hipSuccess) return hip_fail(ctx, e, "norm kernel launch");
     e = timed(ctx, ATTN_K_QKV, s, [&] {
-        return attn_launch_gemv(0, w + L.wqkv_off, h, T, d, L.nqkv, qkv, nullptr, nullptr, s);
+        return attn_launch_qkv(w + L.wqkv_off, h, reinterpret_cast<const double*>(w + L.freq_off),
+                               qkv, q, layer_k(ctx, layer), layer_v(ctx, layer), T, d, c.n_heads,
+                               c.n_kv_heads, c.head_dim, c.max_seq, pos0, s);
     });
     if (e != hipSuccess) return hip_fail(ctx, e, "projection kernel launch");
-    e = timed(ctx, ATTN_K_ROPE, s, [&] {
-        return attn_launch_rope(qkv, q, layer_k(ctx, layer), layer_v(ctx, layer), T, c.n_heads,
-                                c.n_kv_heads, c.head_dim, c.max_seq, pos0, (double)c.rope_theta, s);
-    });
-    if (e != hipSuccess) return hip_fail(ctx, e, "rotary kernel launch");
     e = timed(ctx, ATTN_K_SCORE, s, [&] {
-        return attn_launch_attention(q, layer_k(ctx, layer), layer_v(ctx, layer), part, a, T,
-                                     c.n_heads, c.n_kv_heads, c.head_dim, c.max_seq, pos0,
-                                     L.n_chunks, s);
+        return attn_launch_score(q, layer_k(ctx, layer), layer_v(ctx, layer), part, T, c.n_heads,
+                                 c.n_kv_heads, c.head_dim, c.max_seq, pos0, L.n_chunks, s);
     });
     if (e != hipSuccess) return hip_fail(ctx, e, "attention kernel launch");
+    e = timed(ctx, ATTN_K_COMBINE, s, [&] {
+        return attn_launch_combine(part, a, T, c.n_heads, c.head_dim, pos0, L.n_chunks, s);
+    });
+    if (e != hipSuccess) return hip_fail(ctx, e, "merge kernel launch");
     e = timed(ctx, ATTN_K_OUT, s, [&] {
-        return attn_launch_gemv(1, w + L.wo_off, a, T, L.nq, d, o, x, y, s);
+        return attn_launch_out(w + L.wo_off, a, T, L.nq, d, o, x, y, s);
     });
     if (e != hipSuccess) return hip_fail(ctx, e, "output projection kernel launch");
     return MOE_OK;

@@ -34,6 +34,17 @@ constexpr int kTileK = 32;
 constexpr int kTileBytes = kTileRows * kTileK * 2;  // 1 KiB
 constexpr int kWave = 64;
 
+// Packed row of feature n of a matrix whose rows come in heads of width hd
+// (a multiple of 32) to be rotated in pairs (i, i + hd/2): tile m of a head
+// holds features 8m .. 8m+7 in rows 0..7 and hd/2 + 8m .. +7 in rows 8..15,
+// so both members of a pair sit in one 16-row tile, 8 rows apart.
+__host__ __device__ inline int rope_row(int n, int hd)
+{
+    const int i = n % hd, half = hd / 2;
+    const int r = i < half ? (i / 8) * 16 + i % 8 : ((i - half) / 8) * 16 + 8 + (i - half) % 8;
+    return n - i + r;
+}
+
 // Byte offset of (row tile rt, K tile kt) for a matrix with KT K tiles.
 __host__ __device__ inline uint64_t tile_offset(uint64_t rt, uint64_t kt, uint64_t KT)
 {
@@ -122,6 +133,10 @@ extern "C" {
 hipError_t moe_launch_pack(const uint16_t* src, int K, int N, void* dst, int rt_mul, int rt_add,
                            hipStream_t s);
 void moe_pack_host(const uint16_t* src, int K, int N, uint8_t* dst, int rt_mul, int rt_add);
+hipError_t moe_launch_pack_perm(const uint16_t* src, int K, int N, void* dst, int rt_mul,
+                                int rt_add, int perm_hd, int perm_rows, hipStream_t s);
+void moe_pack_host_perm(const uint16_t* src, int K, int N, uint8_t* dst, int rt_mul, int rt_add,
+                        int perm_hd, int perm_rows);
 int moe_route_decode_ok(int T, int E, int k);
 int moe_route_decode_wgs(int d);
 hipError_t moe_launch_route_decode(const uint16_t* x, const float* wrT, const float* bias,
@@ -147,14 +162,16 @@ hipError_t moe_launch_combine(const float* O, const int32_t* pair_row, const flo
 extern "C" {
 hipError_t attn_launch_norm(const uint16_t* x, const float* gamma, int T, int d, float eps,
                             uint16_t* h, hipStream_t s);
-hipError_t attn_launch_gemv(int out_mode, const void* w, const uint16_t* x, int T, int K, int N,
-                            float* y32, const uint16_t* res, uint16_t* y16, hipStream_t s);
-hipError_t attn_launch_rope(const float* qkv, uint16_t* q, uint16_t* kc, uint16_t* vc, int T,
-                            int H, int G, int hd, int max_seq, int pos0, double theta,
-                            hipStream_t s);
+hipError_t attn_launch_qkv(const void* w, const uint16_t* h, const double* inv_freq, float* qkv,
+                           uint16_t* q, uint16_t* kc, uint16_t* vc, int T, int d, int H, int G,
+                           int hd, int max_seq, int pos0, hipStream_t s);
+hipError_t attn_launch_out(const void* w, const uint16_t* x, int T, int K, int N, float* y32,
+                           const uint16_t* res, uint16_t* y16, hipStream_t s);
 int attn_chunks(int n_pos);
 int attn_part_stride(int hd);
-hipError_t attn_launch_attention(const uint16_t* q, const uint16_t* kc, const uint16_t* vc,
-                                 float* part, uint16_t* out, int T, int H, int G, int hd,
-                                 int max_seq, int pos0, int n_chunks_alloc, hipStream_t s);
+hipError_t attn_launch_score(const uint16_t* q, const uint16_t* kc, const uint16_t* vc,
+                             float* part, int T, int H, int G, int hd, int max_seq, int pos0,
+                             int n_chunks_alloc, hipStream_t s);
+hipError_t attn_launch_combine(const float* part, uint16_t* out, int T, int H, int hd, int pos0,
+                               int n_chunks_alloc, hipStream_t s);
 }

@@ -11,10 +11,11 @@
 namespace moe {
 
 // One block repacks src[k0:k0+64][n0:n0+64].  Feature n lands in row tile
-// (n/16)*rt_mul + rt_add of the destination, which has KT = K/32 K tiles.
+// (n'/16)*rt_mul + rt_add of the destination, which has KT = K/32 K tiles;
+// n' = n, or rope_row(n) for the features below perm_rows.
 __global__ __launch_bounds__(256) void pack_kernel(const uint16_t* __restrict__ src, int K, int N,
                                                    uint8_t* __restrict__ dst, int rt_mul,
-                                                   int rt_add)
+                                                   int rt_add, int perm_hd, int perm_rows)
 {
     __shared__ uint16_t tile[64][64 + 2];
     const int n0 = blockIdx.x * 64;
@@ -37,6 +38,7 @@ __global__ __launch_bounds__(256) void pack_kernel(const uint16_t* __restrict__ 
         int nl = c & 63;        // feature within block (fastest: contiguous lanes)
         int kg = c >> 6;        // 8-wide K group within the 64-K block (0..7)
         int n = n0 + nl;
+        if (n < perm_rows) n = rope_row(n, perm_hd);
         int kk = kg * 8;        // K offset within block
         u32x4_t w;
 #pragma unroll
@@ -52,27 +54,41 @@ __global__ __launch_bounds__(256) void pack_kernel(const uint16_t* __restrict__ 
 
 }  // namespace moe
 
-extern "C" hipError_t moe_launch_pack(const uint16_t* src, int K, int N, void* dst, int rt_mul,
-                                      int rt_add, hipStream_t s)
+extern "C" hipError_t moe_launch_pack_perm(const uint16_t* src, int K, int N, void* dst,
+                                           int rt_mul, int rt_add, int perm_hd, int perm_rows,
+                                           hipStream_t s)
 {
     dim3 grid(N / 64, K / 64);
     hipLaunchKernelGGL(moe::pack_kernel, grid, dim3(256), 0, s, src, K, N, (uint8_t*)dst, rt_mul,
-                       rt_add);
+                       rt_add, perm_hd, perm_rows);
     return hipGetLastError();
 }
 
+extern "C" hipError_t moe_launch_pack(const uint16_t* src, int K, int N, void* dst, int rt_mul,
+                                      int rt_add, hipStream_t s)
+{
+    return moe_launch_pack_perm(src, K, N, dst, rt_mul, rt_add, 0, 0, s);
+}
+
 // The same repack on the host, for weights that arrive in host memory.
-extern "C" void moe_pack_host(const uint16_t* src, int K, int N, uint8_t* dst, int rt_mul,
-                              int rt_add)
+extern "C" void moe_pack_host_perm(const uint16_t* src, int K, int N, uint8_t* dst, int rt_mul,
+                                   int rt_add, int perm_hd, int perm_rows)
 {
     const uint64_t KT = (uint64_t)K / moe::kTileK;
-    for (int n = 0; n < N; ++n) {
+    for (int n0 = 0; n0 < N; ++n0) {
+        const int n = n0 < perm_rows ? moe::rope_row(n0, perm_hd) : n0;
         const uint64_t rt = (uint64_t)(n / moe::kTileRows) * rt_mul + rt_add;
         for (int k0 = 0; k0 < K; k0 += 8) {
             const uint64_t kt = (uint64_t)k0 / moe::kTileK;
             const int lane = ((k0 % moe::kTileK) / 8) * 16 + (n % moe::kTileRows);
             uint16_t* p = reinterpret_cast<uint16_t*>(dst + moe::tile_offset(rt, kt, KT) + lane * 16);
-            for (int i = 0; i < 8; ++i) p[i] = src[(size_t)(k0 + i) * N + n];
+            for (int i = 0; i < 8; ++i) p[i] = src[(size_t)(k0 + i) * N + n0];
         }
     }
+}
+
+extern "C" void moe_pack_host(const uint16_t* src, int K, int N, uint8_t* dst, int rt_mul,
+                              int rt_add)
+{
+    moe_pack_host_perm(src, K, N, dst, rt_mul, rt_add, 0, 0);
 }

@@ -244,13 +244,13 @@ def _attn_cfg(**kw):
 
 def test_attn_sizes():
     cfg = _attn_cfg()
-    layer = 6144 * 4 + (6144 * 8192 + 6144 * 6144) * 2     # gamma, Wqkv, Wo
+    layer = 6144 * 4 + 512 + (6144 * 8192 + 6144 * 6144) * 2     # gamma, frequencies, Wqkv, Wo
     assert moe.attn_weight_bytes(cfg) == layer
     assert moe.attn_cache_bytes(_attn_cfg(n_layers=3)) == 3 * 2 * 8 * 4096 * 128 * 2
     assert moe.attn_workspace_bytes(cfg) > 16 * (6144 * 2 + 8192 * 4)
 
 
-@pytest.mark.parametrize("bad", [dict(d_model=200), dict(head_dim=96), dict(n_kv_heads=5),
+@pytest.mark.parametrize("bad", [dict(d_model=200), dict(d_model=8448), dict(head_dim=96), dict(n_kv_heads=5),
                                  dict(n_heads=64, n_kv_heads=4), dict(max_tokens=17),
                                  dict(max_tokens=0), dict(max_seq=0), dict(n_layers=0),
                                  dict(rope_theta=1.0), dict(norm_eps=-1.0), dict(flags=1),
