@@ -1,8 +1,10 @@
 // attn.hip -- kernels of the self-attention block of include/attn.h for a few
 // new tokens (T <= 16: decode), in launch order:
 //
-//   norm_kernel     layer norm, one workgroup per token (one pass, fp64
-//                   sums, fixed reduction order), h = bf16((x - mean) rstd gamma)
+//   norm_kernel     layer norm for more than 4 tokens, one workgroup per
+//                   token (one pass, fp64 sums, fixed reduction order),
+//                   h = bf16((x - mean) rstd gamma); up to 4 tokens the
+//                   projection forms h itself
 //   qkv_kernel      q|k|v = h Wqkv, and in its epilogue the rotary encoding
 //                   of the query and key heads (angles reduced in fp64,
 //                   rotation in fp32): bf16 q to the workspace, bf16 k and v
@@ -171,7 +173,11 @@ __global__ __launch_bounds__(kNormThreads) void norm_kernel(const uint16_t* __re
 // pos0 + j; the unrotated fp32 values are kept for inspection.
 struct QkvArgs {
     const uint8_t* w;      // packed Wqkv, query and key heads permuted by rope_row
-    const uint16_t* h;     // [T][d] bf16, the normalised input
+    const uint16_t* h;     // [T][d] bf16, the normalised input (written here when the
+                           // kernel normalises x itself)
+    const uint16_t* x;     // [T][d] bf16 block input (normalising kernel only)
+    const float* gamma;    // [d]
+    float eps;
     const double* inv_freq;  // [hd/2]: theta^(-2f/hd)
     float* qkv;            // [T][nqkv] fp32, natural order, before rotation
     uint16_t* q;           // [T][H][hd]
@@ -194,34 +200,146 @@ __device__ inline void rope_cs(int pos, double inv_freq, float& c, float& s)
     sincosf((float)r, &s, &c);
 }
 
+// barrier for LDS traffic only: waits for this wave's LDS operations, not
+// for its outstanding global loads (the weight batch in flight)
+__device__ __forceinline__ void lds_barrier()
+{
+    constexpr int kWaitLgkm = 0xC07F;   // lgkmcnt 0; vmcnt and expcnt at their maxima
+    asm volatile("" ::: "memory");
+    __builtin_amdgcn_s_waitcnt(kWaitLgkm);
+    __builtin_amdgcn_s_barrier();
+    asm volatile("" ::: "memory");
+}
+
+constexpr int kLnMaxT = 4;     // tokens up to which the projection normalises x itself
+constexpr int kLnGroups = 2;   // 8-element groups per thread and token (d <= 8192)
+constexpr int kHPad = 8;       // bf16 padding of a token row of h in LDS
+
+// kNorm (T <= kLnMaxT): every workgroup forms the layer norm of the T tokens
+// itself, into LDS, while its first weight batch is in flight -- x and gamma
+// loaded first (thread i: 8-element groups i and i + 512), then the weights,
+// then x and x^2 summed in fp64 (butterfly per wave, the 8 waves in order),
+// h = bf16((x - mean) rstd gamma) to LDS (workgroup 0 also writes it out);
+// the main loop then reads its B fragments from LDS.  Otherwise h comes from
+// norm_kernel through global memory.
+template <bool kNorm>
 __global__ __launch_bounds__(64 * kSplit) void qkv_kernel(QkvArgs a)
 {
     __shared__ f32x4_t s_red[(kSplit - 1) * 64];
+    extern __shared__ __attribute__((aligned(16))) uint16_t hs[];   // kNorm: [T][d + kHPad]
     const int q = blockIdx.x;
     const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
     const int j = lane & 15, g = lane >> 4;
     const int KT = a.d / kTileK;
+    const int hstride = a.d + kHPad;
     const uint8_t* pw = a.w + moe::tile_offset(q, 0, KT) + lane * 16;
     const bool has_tok = j < a.T;
     const uint16_t* px = a.h + (has_tok ? (int64_t)j * a.d : 0) + g * 8;
+    const uint16_t* hx = hs + (has_tok ? j * hstride : 0) + g * 8;
     f32x4_t acc = {0.f, 0.f, 0.f, 0.f};
     const u32x4_t zero = {0u, 0u, 0u, 0u};
+    u32x4_t wv[kUnroll], xb[kUnroll];
+    if constexpr (kNorm) {
+        __shared__ double red[2][kLnMaxT][kSplit];
+        const int tid = threadIdx.x, ng = a.d / 8;
+        u32x4_t xv[kLnMaxT][kLnGroups];
+        float4 gv[kLnGroups][2];
+        // unconditional loads (indices clamped, values masked after): no
+        // branch between them and the weight batch, so the first use of x
+        // waits for x alone
+#pragma unroll
+        for (int t = 0; t < kLnMaxT; ++t)
+#pragma unroll
+            for (int k = 0; k < kLnGroups; ++k) {
+                const int e = tid + k * 64 * kSplit;
+                const u32x4_t v = ld16(a.x + (int64_t)min(t, a.T - 1) * a.d + min(e, ng - 1) * 8);
+                xv[t][k] = t < a.T && e < ng ? v : zero;
+            }
+#pragma unroll
+        for (int k = 0; k < kLnGroups; ++k) {
+            const int e = min(tid + k * 64 * kSplit, ng - 1);
+            gv[k][0] = *reinterpret_cast<const float4*>(a.gamma + e * 8);
+            gv[k][1] = *reinterpret_cast<const float4*>(a.gamma + e * 8 + 4);
+        }
+        // the first batch (tile indices clamped, so that the loads need no
+        // branch; below 64 K tiles the values go unused)
+#pragma unroll
+        for (int u = 0; u < kUnroll; ++u)
+            wv[u] = ld16_nt(pw + (int64_t)min(w + kSplit * u, KT - 1) * kTileBytes);
+#pragma unroll
+        for (int t = 0; t < kLnMaxT; ++t) {
+            if (t >= a.T) break;
+            double sx = 0.0, sq = 0.0;
+#pragma unroll
+            for (int k = 0; k < kLnGroups; ++k)
+#pragma unroll
+                for (int i = 0; i < 4; ++i) {
+                    const double lo = __uint_as_float(xv[t][k][i] << 16);
+                    const double hi = __uint_as_float(xv[t][k][i] & 0xFFFF0000u);
+                    sx += lo + hi;
+                    sq = fma(lo, lo, fma(hi, hi, sq));
+                }
+            for (int off = 32; off >= 1; off >>= 1) {
+                sx += __shfl_xor(sx, off, 64);
+                sq += __shfl_xor(sq, off, 64);
+            }
+            if (lane == 0) { red[0][t][w] = sx; red[1][t][w] = sq; }
+        }
+        lds_barrier();
+#pragma unroll
+        for (int t = 0; t < kLnMaxT; ++t) {
+            if (t >= a.T) break;
+            double m1 = 0.0, m2 = 0.0;
+#pragma unroll
+            for (int i = 0; i < kSplit; ++i) { m1 += red[0][t][i]; m2 += red[1][t][i]; }
+            const double mean = m1 / a.d;
+            const float rstd = (float)(1.0 / sqrt(fmax(m2 / a.d - mean * mean, 0.0) + (double)a.eps));
+            const float mu = (float)mean;
+#pragma unroll
+            for (int k = 0; k < kLnGroups; ++k) {
+                const int e = tid + k * 64 * kSplit;
+                if (e >= ng) break;
+                const float gm[8] = {gv[k][0].x, gv[k][0].y, gv[k][0].z, gv[k][0].w,
+                                     gv[k][1].x, gv[k][1].y, gv[k][1].z, gv[k][1].w};
+                u32x4_t out;
+#pragma unroll
+                for (int i = 0; i < 4; ++i) {
+                    const float lo = (__uint_as_float(xv[t][k][i] << 16) - mu) * rstd * gm[2 * i];
+                    const float hi = (__uint_as_float(xv[t][k][i] & 0xFFFF0000u) - mu) * rstd * gm[2 * i + 1];
+                    out[i] = (uint32_t)moe::f32_to_bf16(lo) | ((uint32_t)moe::f32_to_bf16(hi) << 16);
+                }
+                *reinterpret_cast<u32x4_t*>(hs + t * hstride + e * 8) = out;
+                if (q == 0) *reinterpret_cast<u32x4_t*>(const_cast<uint16_t*>(a.h) + (int64_t)t * a.d + e * 8) = out;
+            }
+        }
+        lds_barrier();
+    }
     int kt = 0;
     for (; kt + kSplit * kUnroll <= KT; kt += kSplit * kUnroll) {
-        u32x4_t wv[kUnroll], xb[kUnroll];
+        if (!kNorm || kt > 0) {
 #pragma unroll
-        for (int u = 0; u < kUnroll; ++u)
-            wv[u] = ld16_nt(pw + (int64_t)(kt + w + kSplit * u) * kTileBytes);
+            for (int u = 0; u < kUnroll; ++u)
+                wv[u] = ld16_nt(pw + (int64_t)(kt + w + kSplit * u) * kTileBytes);
+        }
 #pragma unroll
-        for (int u = 0; u < kUnroll; ++u)
-            xb[u] = has_tok ? ld16(px + (kt + w + kSplit * u) * kTileK) : zero;
+        for (int u = 0; u < kUnroll; ++u) {
+            const int ko = (kt + w + kSplit * u) * kTileK;
+            if constexpr (kNorm)
+                xb[u] = has_tok ? *reinterpret_cast<const u32x4_t*>(hx + ko) : zero;
+            else
+                xb[u] = has_tok ? ld16(px + ko) : zero;
+        }
 #pragma unroll
         for (int u = 0; u < kUnroll; ++u) acc = moe::mfma16x16x32(wv[u], xb[u], acc);
     }
     for (kt += w; kt < KT; kt += kSplit) {
-        const u32x4_t wv = ld16_nt(pw + (int64_t)kt * kTileBytes);
-        const u32x4_t xb = has_tok ? ld16(px + kt * kTileK) : zero;
-        acc = moe::mfma16x16x32(wv, xb, acc);
+        const u32x4_t wt = ld16_nt(pw + (int64_t)kt * kTileBytes);
+        u32x4_t xt;
+        if constexpr (kNorm)
+            xt = has_tok ? *reinterpret_cast<const u32x4_t*>(hx + kt * kTileK) : zero;
+        else
+            xt = has_tok ? ld16(px + kt * kTileK) : zero;
+        acc = moe::mfma16x16x32(wt, xt, acc);
     }
     if (w > 0) s_red[(w - 1) * 64 + lane] = acc;
     __syncthreads();
@@ -464,15 +582,23 @@ hipError_t attn_launch_norm(const uint16_t* x, const float* gamma, int T, int d,
     return hipGetLastError();
 }
 
-hipError_t attn_launch_qkv(const void* w, const uint16_t* h, const double* inv_freq, float* qkv,
-                           uint16_t* q, uint16_t* kc, uint16_t* vc, int T, int d, int H, int G,
-                           int hd, int max_seq, int pos0, hipStream_t s)
+int attn_norm_in_projection(int T) { return T <= attn::kLnMaxT; }
+
+hipError_t attn_launch_qkv(const void* w, uint16_t* h, const uint16_t* x, const float* gamma,
+                           float eps, const double* inv_freq, float* qkv, uint16_t* q,
+                           uint16_t* kc, uint16_t* vc, int T, int d, int H, int G, int hd,
+                           int max_seq, int pos0, hipStream_t s)
 {
-    attn::QkvArgs a{static_cast<const uint8_t*>(w), h, inv_freq, qkv, q, kc, vc,
+    attn::QkvArgs a{static_cast<const uint8_t*>(w), h, x, gamma, eps, inv_freq, qkv, q, kc, vc,
                     d, T, H, G, hd, max_seq, pos0};
     const int rows = (H + 2 * G) * hd;
-    hipLaunchKernelGGL(attn::qkv_kernel, dim3(rows / moe::kTileRows), dim3(64 * attn::kSplit), 0, s,
-                       a);
+    const dim3 grid(rows / moe::kTileRows), block(64 * attn::kSplit);
+    if (attn_norm_in_projection(T)) {
+        const size_t lds = (size_t)T * (d + attn::kHPad) * 2;
+        hipLaunchKernelGGL(attn::qkv_kernel<true>, grid, block, lds, s, a);
+    } else {
+        hipLaunchKernelGGL(attn::qkv_kernel<false>, grid, block, 0, s, a);
+    }
     return hipGetLastError();
 }
 

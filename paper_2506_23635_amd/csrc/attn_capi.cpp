@@ -1,9 +1,9 @@
 // attn_capi.cpp -- the C-ABI of include/attn.h: configuration checks, the
 // carve-up of the caller's weight arena, cache and workspace, the one-time
 // weight repack (the query and key heads of Wqkv with their rotation pairs
-// in one tile), and the launch sequence of the block (norm -> fused
-// projection + rotary + cache append -> attention over position chunks ->
-// merge -> output projection + residual).  Nothing here allocates device
+// in one tile), and the launch sequence of the block (norm, inside the
+// projection up to 4 tokens -> fused projection + rotary + cache append ->
+// attention over position chunks -> merge -> output projection + residual).  Nothing here allocates device
 // memory.
 #include <hip/hip_runtime.h>
 
@@ -267,13 +267,18 @@ moe_status attn_forward(attn_ctx* ctx, int32_t layer, const uint16_t* x, uint16_
     uint16_t* a = reinterpret_cast<uint16_t*>(ctx->ws + L.a_off);
     float* o = reinterpret_cast<float*>(ctx->ws + L.o_off);
     const int d = c.d_model;
-    hipError_t e = timed(ctx, ATTN_K_NORM, s, [&] {
-        return attn_launch_norm(x, reinterpret_cast<const float*>(w), T, d, c.norm_eps, h, s);
-    });
-    if (e != hipSuccess) return hip_fail(ctx, e, "norm kernel launch");
+    const float* gamma = reinterpret_cast<const float*>(w);
+    hipError_t e = hipSuccess;
+    if (!attn_norm_in_projection(T)) {
+        e = timed(ctx, ATTN_K_NORM, s, [&] {
+            return attn_launch_norm(x, gamma, T, d, c.norm_eps, h, s);
+        });
+        if (e != hipSuccess) return hip_fail(ctx, e, "norm kernel launch");
+    }
     e = timed(ctx, ATTN_K_QKV, s, [&] {
-        return attn_launch_qkv(w + L.wqkv_off, h, reinterpret_cast<const double*>(w + L.freq_off),
-                               qkv, q, layer_k(ctx, layer), layer_v(ctx, layer), T, d, c.n_heads,
+        return attn_launch_qkv(w + L.wqkv_off, h, x, gamma, c.norm_eps,
+                               reinterpret_cast<const double*>(w + L.freq_off), qkv, q,
+                               layer_k(ctx, layer), layer_v(ctx, layer), T, d, c.n_heads,
                                c.n_kv_heads, c.head_dim, c.max_seq, pos0, s);
     });
     if (e != hipSuccess) return hip_fail(ctx, e, "projection kernel launch");

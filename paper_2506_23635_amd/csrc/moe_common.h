@@ -162,9 +162,11 @@ hipError_t moe_launch_combine(const float* O, const int32_t* pair_row, const flo
 extern "C" {
 hipError_t attn_launch_norm(const uint16_t* x, const float* gamma, int T, int d, float eps,
                             uint16_t* h, hipStream_t s);
-hipError_t attn_launch_qkv(const void* w, const uint16_t* h, const double* inv_freq, float* qkv,
-                           uint16_t* q, uint16_t* kc, uint16_t* vc, int T, int d, int H, int G,
-                           int hd, int max_seq, int pos0, hipStream_t s);
+int attn_norm_in_projection(int T);
+hipError_t attn_launch_qkv(const void* w, uint16_t* h, const uint16_t* x, const float* gamma,
+                           float eps, const double* inv_freq, float* qkv, uint16_t* q,
+                           uint16_t* kc, uint16_t* vc, int T, int d, int H, int G, int hd,
+                           int max_seq, int pos0, hipStream_t s);
 hipError_t attn_launch_out(const void* w, const uint16_t* x, int T, int K, int N, float* y32,
                            const uint16_t* res, uint16_t* y16, hipStream_t s);
 int attn_chunks(int n_pos);

@@ -121,7 +121,7 @@ def test_route_from_x_many_tokens(torch_mod, tiny_layer, T):
     _check_routing(got, idx, w, wl.E)
 
 
-@pytest.mark.parametrize("T", [1, 7, 16])
+@pytest.mark.parametrize("T", [1, 4, 5, 16])
 def test_decode_routing_ties(torch_mod, tiny_layer, T):
     """A zero router weight makes every logit equal to its expert's bias, so
     the decode routing must break ties by the lower expert id (and order the
@@ -142,12 +142,14 @@ def test_decode_routing_ties(torch_mod, tiny_layer, T):
     layer.close()
 
 
-def test_decode_routing_nan_token(torch_mod, tiny_layer):
+@pytest.mark.parametrize("T", [4, 8])
+def test_decode_routing_nan_token(torch_mod, tiny_layer, T):
     """A token whose activations hold a NaN has NaN logits (the oracle rejects
     such rows, so no reference exists for them): it still gets k distinct
-    valid experts, and the other tokens route exactly as the oracle says."""
+    valid experts, and the other tokens route exactly as the oracle says
+    (T = 4: one routing workgroup; T = 8: partial logits over several)."""
     torch = torch_mod
-    wl = TINY.with_(T=4)
+    wl = TINY.with_(T=T)
     x = wl.x().copy()
     x[2, 5] = 0x7FC0                       # bf16 quiet NaN
     x_t = torch.from_numpy(x.view(np.int16)).cuda()
@@ -155,7 +157,7 @@ def test_decode_routing_nan_token(torch_mod, tiny_layer):
     assert np.isnan(got["logits"][2]).all()
     ids = got["idx"][2]
     assert len(set(ids.tolist())) == wl.k and ids.min() >= 0 and ids.max() < wl.E
-    ok = np.array([0, 1, 3])
+    ok = np.array([t for t in range(T) if t != 2])
     lg = oracle.router_logits(x[ok], wl.router())
     idx, w = oracle.route_from_logits(lg, wl.k)
     assert np.array_equal(got["idx"][ok], idx)
@@ -265,7 +267,7 @@ def _chain(torch, layer, wl, x, x_t, y, e_begin=0, n_local=0, y_f32=False):
                        lambda e: (G[e], U[e], D[e]), y_f32=y_f32)
 
 
-@pytest.mark.parametrize("T", [1, 5, 16])
+@pytest.mark.parametrize("T", [1, 2, 5, 16])
 def test_forward_decode_path(torch_mod, tiny_layer, T):
     torch = torch_mod
     wl = TINY.with_(T=T)
@@ -275,6 +277,28 @@ def test_forward_decode_path(torch_mod, tiny_layer, T):
     check_layer_output(y, ref["y64"])
     st = _chain(torch, tiny_layer, wl, x, x_t, y)
     assert st["rows"] == T * wl.k
+
+
+@pytest.mark.parametrize("T", [1, 2, 3])
+def test_forward_leaves_the_routing_of_moe_route(torch_mod, tiny_layer, T):
+    """A forward without a routing argument routes itself: the views it
+    leaves equal moe_route's bit for bit.  Route x, forward another x (the
+    views change), forward x again and read the same views."""
+    torch = torch_mod
+    wl = TINY.with_(T=T)
+    x_t, x = x_device(wl)
+    x2_t, _ = x_device(wl, layer_idx=1)
+    r = tiny_layer.route(0, x_t)
+    want = tiny_layer.routing_tensors(r)
+    y = torch.empty((T, wl.d), dtype=torch.int16, device="cuda")
+    tiny_layer.forward(0, x2_t, y)
+    other = tiny_layer.routing_tensors(r)
+    assert not np.array_equal(other["logits"].view(np.uint32), want["logits"].view(np.uint32))
+    tiny_layer.forward(0, x_t, y)
+    got = tiny_layer.routing_tensors(r)
+    for key in want:
+        assert np.array_equal(np.asarray(got[key]).view(np.uint8),
+                              np.asarray(want[key]).view(np.uint8)), key
 
 
 @pytest.mark.parametrize("T", [17, 100, 300, 512])
