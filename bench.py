@@ -520,7 +520,9 @@ def attn_section(steps, warmup, n_rot=N_ROT):
     wqkv_b, wo_b = wl.d * wl.nqkv * 2, wl.n_heads * wl.hd * wl.d * 2
     kv_b = 2 * wl.n_kv * (pos0 + 1) * wl.hd * 2
     step_b = wqkv_b + wo_b + wl.d * 4 + kv_b + 2 * wl.d * 2
-    qkv_b = wqkv_b + wl.d * 2
+    # the projection's own bytes: Wqkv, x and gamma (it forms the norm
+    # itself at T = 1) and the bf16 q, k, v it writes
+    qkv_b = wqkv_b + wl.d * 2 + wl.d * 4 + wl.nqkv * 2
     best = min(ms, ms_graph)
     out = {"workload": "dbrx_attention_decode", "T": 1, "context": pos0 + 1,
            "rotation_layers": n_rot, "us_per_layer": best * 1e3, "us_direct_launch": ms * 1e3,
@@ -530,6 +532,7 @@ def attn_section(steps, warmup, n_rot=N_ROT):
            "roofline": {"bound": "hbm", "kernel": "qkv", "achieved": qkv_b / (kern["qkv"] * 1e-6) / 1e9,
                         "peak": HBM_PEAK_GBS, "unit": "GB/s",
                         "frac": qkv_b / (kern["qkv"] * 1e-6) / 1e9 / HBM_PEAK_GBS,
+                        "traffic": measured_traffic("attn_qkv", "attn.hip"),
                         "algorithmic_bytes": qkv_b}}
     log(f"attention decode: {best * 1e3:.1f} us/layer ({out['hbm_gbs']:.0f} GB/s), kernels {kern}")
     layer.close()
