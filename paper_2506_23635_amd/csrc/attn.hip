@@ -68,22 +68,57 @@ __global__ __launch_bounds__(64 * kSplit) void gemv_kernel(GemvArgs a)
     const uint16_t* px = a.x + (has_tok ? (int64_t)j * a.K : 0) + g * 8;
     f32x4_t acc = {0.f, 0.f, 0.f, 0.f};
     const u32x4_t zero = {0u, 0u, 0u, 0u};
+    constexpr int kStep = kSplit * kUnroll;
+    const int nb = KT / kStep;                 // full batches of kUnroll tiles per wave
+    // token loads without branches (an unused column reads token 0's row and
+    // feeds zeros), so that a wait for them is not a wait for everything
+    auto xload = [&](int k0, u32x4_t* xv) {
+#pragma unroll
+        for (int u = 0; u < kUnroll; ++u) {
+            const u32x4_t v = ld16(px + (k0 + w + kSplit * u) * kTileK);
+            xv[u] = has_tok ? v : zero;
+        }
+    };
+    auto wload = [&](int k0, u32x4_t* wt) {
+#pragma unroll
+        for (int u = 0; u < kUnroll; ++u)
+            wt[u] = ld16_nt(pw + (int64_t)(k0 + w + kSplit * u) * kTileBytes);
+    };
+    auto mfmas = [&](const u32x4_t* wt, const u32x4_t* xv) {
+#pragma unroll
+        for (int u = 0; u < kUnroll; ++u) acc = moe::mfma16x16x32(wt[u], xv[u], acc);
+    };
     int kt = 0;
-    for (; kt + kSplit * kUnroll <= KT; kt += kSplit * kUnroll) {
-        u32x4_t wv[kUnroll], xb[kUnroll];
-#pragma unroll
-        for (int u = 0; u < kUnroll; ++u)
-            wv[u] = ld16_nt(pw + (int64_t)(kt + w + kSplit * u) * kTileBytes);
-#pragma unroll
-        for (int u = 0; u < kUnroll; ++u)
-            xb[u] = has_tok ? ld16(px + (kt + w + kSplit * u) * kTileK) : zero;
-#pragma unroll
-        for (int u = 0; u < kUnroll; ++u) acc = moe::mfma16x16x32(wv[u], xb[u], acc);
+    if (nb > 0) {
+        // two weight buffers in turn: the next batch's weights are issued
+        // after this batch's token loads and before its MFMAs, so they stay
+        // in flight while it is multiplied
+        u32x4_t wa[kUnroll], wb[kUnroll], xv[kUnroll];
+        wload(0, wa);
+        int b = 0;
+        for (; b + 2 < nb; b += 2) {
+            xload(b * kStep, xv);
+            wload((b + 1) * kStep, wb);
+            mfmas(wa, xv);
+            xload((b + 1) * kStep, xv);
+            wload((b + 2) * kStep, wa);
+            mfmas(wb, xv);
+        }
+        xload(b * kStep, xv);
+        if (b + 1 < nb) {
+            wload((b + 1) * kStep, wb);
+            mfmas(wa, xv);
+            xload((b + 1) * kStep, xv);
+            mfmas(wb, xv);
+        } else {
+            mfmas(wa, xv);
+        }
+        kt = nb * kStep;
     }
     for (kt += w; kt < KT; kt += kSplit) {
-        const u32x4_t wv = ld16_nt(pw + (int64_t)kt * kTileBytes);
-        const u32x4_t xb = has_tok ? ld16(px + kt * kTileK) : zero;
-        acc = moe::mfma16x16x32(wv, xb, acc);
+        const u32x4_t wt = ld16_nt(pw + (int64_t)kt * kTileBytes);
+        const u32x4_t xt = has_tok ? ld16(px + kt * kTileK) : zero;
+        acc = moe::mfma16x16x32(wt, xt, acc);
     }
     if (w > 0) s_red[(w - 1) * 64 + lane] = acc;
     __syncthreads();
@@ -314,23 +349,54 @@ __global__ __launch_bounds__(64 * kSplit) void qkv_kernel(QkvArgs a)
         }
         lds_barrier();
     }
+    // two weight buffers in turn, as gemv_kernel (with kNorm the first batch
+    // was issued above, into wv)
+    constexpr int kStep = kSplit * kUnroll;
+    const int nb = KT / kStep;
     int kt = 0;
-    for (; kt + kSplit * kUnroll <= KT; kt += kSplit * kUnroll) {
-        if (!kNorm || kt > 0) {
-#pragma unroll
-            for (int u = 0; u < kUnroll; ++u)
-                wv[u] = ld16_nt(pw + (int64_t)(kt + w + kSplit * u) * kTileBytes);
-        }
+    auto xload = [&](int k0, u32x4_t* xv) {
 #pragma unroll
         for (int u = 0; u < kUnroll; ++u) {
-            const int ko = (kt + w + kSplit * u) * kTileK;
-            if constexpr (kNorm)
-                xb[u] = has_tok ? *reinterpret_cast<const u32x4_t*>(hx + ko) : zero;
-            else
-                xb[u] = has_tok ? ld16(px + ko) : zero;
+            const int ko = (k0 + w + kSplit * u) * kTileK;
+            if constexpr (kNorm) {
+                xv[u] = has_tok ? *reinterpret_cast<const u32x4_t*>(hx + ko) : zero;
+            } else {
+                const u32x4_t v = ld16(px + ko);
+                xv[u] = has_tok ? v : zero;
+            }
         }
+    };
+    auto wload = [&](int k0, u32x4_t* wt) {
 #pragma unroll
-        for (int u = 0; u < kUnroll; ++u) acc = moe::mfma16x16x32(wv[u], xb[u], acc);
+        for (int u = 0; u < kUnroll; ++u)
+            wt[u] = ld16_nt(pw + (int64_t)(k0 + w + kSplit * u) * kTileBytes);
+    };
+    auto mfmas = [&](const u32x4_t* wt, const u32x4_t* xv) {
+#pragma unroll
+        for (int u = 0; u < kUnroll; ++u) acc = moe::mfma16x16x32(wt[u], xv[u], acc);
+    };
+    if (nb > 0) {
+        u32x4_t wb[kUnroll];
+        if constexpr (!kNorm) wload(0, wv);
+        int b = 0;
+        for (; b + 2 < nb; b += 2) {
+            xload(b * kStep, xb);
+            wload((b + 1) * kStep, wb);
+            mfmas(wv, xb);
+            xload((b + 1) * kStep, xb);
+            wload((b + 2) * kStep, wv);
+            mfmas(wb, xb);
+        }
+        xload(b * kStep, xb);
+        if (b + 1 < nb) {
+            wload((b + 1) * kStep, wb);
+            mfmas(wv, xb);
+            xload((b + 1) * kStep, xb);
+            mfmas(wb, xb);
+        } else {
+            mfmas(wv, xb);
+        }
+        kt = nb * kStep;
     }
     for (kt += w; kt < KT; kt += kSplit) {
         const u32x4_t wt = ld16_nt(pw + (int64_t)kt * kTileBytes);

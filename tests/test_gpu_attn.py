@@ -225,6 +225,25 @@ def test_dbrx_block(torch_mod, T, pos0):
         case.close()
 
 
+@pytest.mark.parametrize("d,H,G,hd,T", [(2048, 32, 8, 64, 2), (2048, 64, 8, 128, 1),
+                                         (4096, 32, 4, 128, 4), (8192, 16, 2, 128, 5)])
+def test_projection_shapes(torch_mod, d, H, G, hd, T):
+    """Widths whose K loops run 1, 2 and 4 full weight batches per wave in
+    the two projections (K = 2048, 4096, 8192 for q|k|v; 2048, 4096, 8192
+    for the output), besides the 0 of the small block and the 3 of the DBRX
+    block; T = 5 takes the separate norm kernel."""
+    torch = torch_mod
+    wl = TINY.with_(d=d, n_heads=H, n_kv=G, hd=hd, T=T, pos0=70)
+    case = Case(torch, wl)
+    try:
+        x = wl.x()
+        y = case.forward(x, wl.pos0)
+        kc, vc = case.cache()
+        check_block(case, x, wl.pos0, y, case.layer.intermediates(T), kc, vc)
+    finally:
+        case.close()
+
+
 def test_in_place_and_rejections(torch_mod):
     torch = torch_mod
     wl = TINY.with_(T=2, pos0=10)
