@@ -97,7 +97,8 @@ typedef struct {
 
 /* Routing of the last moe_route / moe_forward call on a context.  Every
  * pointer is a device view into the workspace, valid until the next
- * moe_route / moe_forward / moe_forward_stack on the same context.
+ * moe_route / moe_forward / moe_forward_stack / moe_forward_layers on the
+ * same context.
  *   logits   fp32 [T, E]      topk_idx int32 [T, k]   topk_w fp32 [T, k]
  *   counts   int32 [E]        pairs routed to each local expert (0 off-share)
  *   offsets  int32 [E + 1]    exclusive prefix sum of counts
@@ -217,6 +218,17 @@ MOE_API moe_status moe_forward_static(moe_ctx *ctx, int32_t layer, const uint16_
  * x_inout is bf16 [T, d].  Requires every layer loaded (MOE_E_STATE). */
 MOE_API moe_status moe_forward_stack(moe_ctx *ctx, uint16_t *x_inout, int32_t T,
                              moe_stream_t stream);
+
+/* Sec. 2.1 (a decoder layer is self-attention followed by the MoE FFN): the
+ * same as moe_forward_stack for the n consecutive layers first .. first+n-1
+ * only, so that a caller can interleave other blocks (the self-attention of
+ * attn.h) between MoE layers: for each of them x = bf16(x + layer_l(x)), in
+ * place, bf16 [T, d].  moe_forward_stack(ctx, x, T, s) is
+ * moe_forward_layers(ctx, 0, n_layers, x, T, s).  Requires 0 <= first,
+ * n >= 0, first + n <= n_layers (MOE_E_ARG) and those layers loaded
+ * (MOE_E_STATE); n == 0 or T == 0 is a no-op. */
+MOE_API moe_status moe_forward_layers(moe_ctx *ctx, int32_t first, int32_t n, uint16_t *x_inout,
+                                      int32_t T, moe_stream_t stream);
 
 /* Workspace map for a caller that owns the workspace and wants to inspect or
  * guard its parts: region i (moe_ws_region order) starts offset[i] bytes

@@ -26,7 +26,7 @@ STATUS_NAMES = {0: "MOE_OK", -1: "MOE_E_ARG", -2: "MOE_E_SHAPE", -3: "MOE_E_ALIG
 EXPORTED = ["moe_weight_bytes", "moe_workspace_bytes", "moe_workspace_map", "moe_init",
             "moe_load_expert",
             "moe_load_router", "moe_route", "moe_forward", "moe_forward_static",
-            "moe_forward_stack",
+            "moe_forward_stack", "moe_forward_layers",
             "moe_intermediates", "moe_profile_enable", "moe_profile_read",
             "moe_profile_gemm_timeline", "moe_destroy",
             "moe_last_error", "moe_status_string", "moe_diag_stream_read",
@@ -99,6 +99,7 @@ def lib():
         L.moe_forward.argtypes = [P, I, P, I, ctypes.POINTER(MoeRouting), P, P]
         L.moe_forward_static.argtypes = [P, I, P, I, P, P]
         L.moe_forward_stack.argtypes = [P, P, I, P]
+        L.moe_forward_layers.argtypes = [P, I, I, P, I, P]
         L.moe_intermediates.argtypes = [P, ctypes.POINTER(P), ctypes.POINTER(P)]
         L.moe_profile_enable.argtypes = [P, I]
         L.moe_profile_read.argtypes = [P, P, P, P]
@@ -128,7 +129,8 @@ def lib():
                    "attn_profile_enable", "attn_profile_read"):
             getattr(L, fn).restype = ctypes.c_int
         for fn in ("moe_init", "moe_load_expert", "moe_load_router", "moe_route", "moe_forward",
-                   "moe_forward_static", "moe_forward_stack", "moe_intermediates", "moe_profile_enable",
+                   "moe_forward_static", "moe_forward_stack", "moe_forward_layers",
+                   "moe_intermediates", "moe_profile_enable",
                    "moe_profile_read", "moe_profile_gemm_timeline", "moe_diag_stream_read"):
             getattr(L, fn).restype = ctypes.c_int
         _lib = L
@@ -198,6 +200,10 @@ def moe_forward_static(ctx, layer, x_ptr, T, y_ptr, stream=0):
 
 def moe_forward_stack(ctx, x_ptr, T, stream=0):
     _check(ctx, lib().moe_forward_stack(ctx, x_ptr, T, stream))
+
+
+def moe_forward_layers(ctx, first, n, x_ptr, T, stream=0):
+    _check(ctx, lib().moe_forward_layers(ctx, first, n, x_ptr, T, stream))
 
 
 def moe_diag_stream_read(src_ptr, nbytes, out_ptr, stream=0):
@@ -374,6 +380,13 @@ class MoeLayer:
         T = self._tokens(x, T)
         moe_forward_stack(self.ctx, _tensor_ptr(x, "x", T * self.cfg.d_model, _bf16_types(self.torch),
                                                 self.device), T, self.stream)
+
+    def forward_layers(self, first, n, x, T=None):
+        """moe_forward_layers: layers first .. first+n-1, x = bf16(x + y) in place."""
+        T = self._tokens(x, T)
+        moe_forward_layers(self.ctx, first, n,
+                           _tensor_ptr(x, "x", T * self.cfg.d_model, _bf16_types(self.torch),
+                                       self.device), T, self.stream)
 
     def routing_tensors(self, r: MoeRouting):
         """Copies the routing views (device) to host numpy arrays."""

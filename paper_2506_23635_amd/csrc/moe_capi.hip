@@ -555,21 +555,24 @@ moe_status moe_forward(moe_ctx* ctx, int32_t layer, const uint16_t* x, int32_t T
                    f32_out ? static_cast<float*>(y) : nullptr, nullptr, s);
 }
 
-moe_status moe_forward_stack(moe_ctx* ctx, uint16_t* x_inout, int32_t T, moe_stream_t stream)
+moe_status moe_forward_layers(moe_ctx* ctx, int32_t first, int32_t n, uint16_t* x_inout,
+                              int32_t T, moe_stream_t stream)
 {
     if (!ctx) return MOE_E_ARG;
+    if (first < 0 || n < 0 || (int64_t)first + n > ctx->cfg.n_layers)
+        return fail(ctx, MOE_E_ARG, "layer range outside [0, n_layers)");
     if (T < 0) return fail(ctx, MOE_E_ARG, "T is negative");
     if (T > ctx->cfg.max_tokens) return fail(ctx, MOE_E_CAPACITY, "T exceeds max_tokens");
-    for (int l = 0; l < ctx->cfg.n_layers; ++l) {
+    for (int l = first; l < first + n; ++l) {
         moe_status st = check_layer(ctx, l);
         if (st != MOE_OK) return st;
     }
-    if (T == 0) return MOE_OK;
+    if (T == 0 || n == 0) return MOE_OK;
     if (!x_inout) return fail(ctx, MOE_E_ARG, "x is NULL");
     if (misaligned(x_inout)) return fail(ctx, MOE_E_ALIGN, "x must be 16-byte aligned");
     hipStream_t s = static_cast<hipStream_t>(stream);
     ctx->route_valid = false;   // the routing views are overwritten layer by layer
-    for (int l = 0; l < ctx->cfg.n_layers; ++l) {
+    for (int l = first; l < first + n; ++l) {
         moe_status st = do_route(ctx, ctx->ws, l, x_inout, T, nullptr, s);
         if (st != MOE_OK) return st;
         st = run_experts(ctx, ctx->ws, l, x_inout, T, s);
@@ -578,6 +581,12 @@ moe_status moe_forward_stack(moe_ctx* ctx, uint16_t* x_inout, int32_t T, moe_str
         if (st != MOE_OK) return st;
     }
     return MOE_OK;
+}
+
+moe_status moe_forward_stack(moe_ctx* ctx, uint16_t* x_inout, int32_t T, moe_stream_t stream)
+{
+    if (!ctx) return MOE_E_ARG;
+    return moe_forward_layers(ctx, 0, ctx->cfg.n_layers, x_inout, T, stream);
 }
 
 moe_status moe_forward_static(moe_ctx* ctx, int32_t layer, const uint16_t* x, int32_t T, void* y,

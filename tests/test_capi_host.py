@@ -147,6 +147,12 @@ def test_ctx_validation_before_any_launch(fake_ctx):
     assert L.moe_forward(fake_ctx, 5, 4096, 1, None, 8192, None) == E_ARG
     assert L.moe_forward(fake_ctx, 0, 4096, 99, None, 8192, None) == E_CAPACITY
     assert L.moe_forward_stack(fake_ctx, 4096, 1, None) == E_STATE
+    assert L.moe_forward_layers(fake_ctx, 0, 1, 4096, 1, None) == E_STATE
+    assert L.moe_forward_layers(fake_ctx, 1, 2, 4096, 1, None) == E_ARG      # past n_layers
+    assert L.moe_forward_layers(fake_ctx, -1, 1, 4096, 1, None) == E_ARG
+    assert L.moe_forward_layers(fake_ctx, 0, -1, 4096, 1, None) == E_ARG
+    assert L.moe_forward_layers(fake_ctx, 0, 0, 4096, 1, None) == 0          # empty range
+    assert L.moe_forward_layers(fake_ctx, 0, 1, 4096, 99, None) == E_CAPACITY
     # experts outside the local range [2, 6), null and misaligned pointers
     assert L.moe_load_expert(fake_ctx, 0, 1, 4096, 4096, 4096, 1, None) == E_ARG
     assert L.moe_load_expert(fake_ctx, 0, 6, 4096, 4096, 4096, 1, None) == E_ARG

@@ -146,8 +146,7 @@ def test_decode_routing_ties(torch_mod, tiny_layer, T):
 def test_decode_routing_nan_token(torch_mod, tiny_layer, T):
     """A token whose activations hold a NaN has NaN logits (the oracle rejects
     such rows, so no reference exists for them): it still gets k distinct
-    valid experts, and the other tokens route exactly as the oracle says
-    (T = 4: one routing workgroup; T = 8: partial logits over several)."""
+    valid experts, and the other tokens route exactly as the oracle says."""
     torch = torch_mod
     wl = TINY.with_(T=T)
     x = wl.x().copy()
@@ -579,6 +578,36 @@ def test_stack_three_layers(torch_mod):
         ref = _oracle_full(wl, cur, layer_idx=li)
         cur = oracle.residual_add(cur, ref["y"])
     assert rel_l2(bf16_f64(got), bf16_f64(cur)) <= 2e-3
+    layer.close()
+
+
+def test_forward_layers_is_the_stack_in_pieces(torch_mod):
+    """moe_forward_layers over ranges that cover the stack equals
+    moe_forward_stack bit for bit; one layer of it is moe_forward followed by
+    the bf16 residual; an empty range leaves x alone."""
+    torch = torch_mod
+    wl = TINY.with_(T=4, n_layers=3)
+    layer = make_layer(wl, max_tokens=4)
+    for li in range(3):
+        load_workload_host(layer, wl, layer_idx=li)
+    x_t, x = x_device(wl)
+    a = x_t.clone()
+    layer.forward_stack(a)
+    b = x_t.clone()
+    layer.forward_layers(0, 1, b)
+    layer.forward_layers(1, 2, b)
+    c = x_t.clone()
+    layer.forward_layers(0, 3, c)
+    d = x_t.clone()
+    layer.forward_layers(1, 1, d)
+    y = torch.empty_like(x_t)
+    layer.forward(1, x_t, y)
+    e = x_t.clone()
+    layer.forward_layers(2, 0, e)
+    torch.cuda.synchronize()
+    assert np.array_equal(to_np_u16(a), to_np_u16(b)) and np.array_equal(to_np_u16(a), to_np_u16(c))
+    assert np.array_equal(to_np_u16(d), oracle.residual_add(x, to_np_u16(y)))
+    assert np.array_equal(to_np_u16(e), x)
     layer.close()
 
 
