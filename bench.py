@@ -385,6 +385,124 @@ def stack_section(steps, warmup):
     return out
 
 
+DECODER_LAYERS = 40     # DBRX's layer count (Table tab:vars)
+
+
+def decoder_bytes():
+    """Pool bytes of the decoder section: the 40 MoE layers' arena and
+    workspace, the 40 attention layers' arena, cache and workspace, and the
+    staging buffers."""
+    import moe_inputs as mi
+    import paper_2506_23635_amd as moe
+    sw = mi.WORKLOADS["stack"].with_(n_layers=DECODER_LAYERS, T=1)
+    aw = mi.ATTN_WORKLOADS["attn_decode"]
+    mcfg = moe.make_config(sw.d, sw.f, sw.E, sw.k, n_layers=DECODER_LAYERS, max_tokens=4)
+    acfg = moe.make_attn_config(aw.d, aw.n_heads, aw.n_kv, aw.hd, n_layers=DECODER_LAYERS,
+                                max_seq=aw.max_seq, max_tokens=4, rope_theta=aw.theta,
+                                norm_eps=aw.eps)
+    return (section_bytes(mcfg, sw) + moe.attn_weight_bytes(acfg) + moe.attn_cache_bytes(acfg) +
+            moe.attn_workspace_bytes(acfg) + (aw.d * aw.nqkv + aw.n_heads * aw.hd * aw.d) * 2 +
+            (64 << 20))
+
+
+def decoder_section(steps, warmup):
+    """A whole DBRX-shaped decoder on one GPU: 40 layers, each the
+    self-attention block (one token after 2047 cached positions) and then
+    the 16-expert MoE layer with its residual (moe_forward_layers), every
+    weight resident (254 GB of experts + 7 GB of attention).  One step is
+    one generated token through all 40 layers; timed with direct launches
+    and as HIP graph replays of the whole step.  HBM bytes per token: the
+    touched experts (4 per layer at T = 1), the routers, and each layer's
+    attention bytes (Wqkv, Wo, gamma, the 2048 positions' keys and values)."""
+    import numpy as np
+    import torch
+    import moe_inputs as mi
+    import paper_2506_23635_amd as moe
+    sw = mi.WORKLOADS["stack"].with_(n_layers=DECODER_LAYERS, T=1)
+    aw = mi.ATTN_WORKLOADS["attn_decode"]
+    need = decoder_bytes()
+    have = _POOL.numel() if _POOL is not None else 0
+    if have < need:
+        log(f"decoder: skipped ({have / 1e9:.0f} GB of pool, {need / 1e9:.0f} GB needed)")
+        return None
+    pool_reset()
+    mcfg = moe.make_config(sw.d, sw.f, sw.E, sw.k, n_layers=DECODER_LAYERS, max_tokens=4)
+    ffn = pool_layer(mcfg)
+    acfg = moe.make_attn_config(aw.d, aw.n_heads, aw.n_kv, aw.hd, n_layers=DECODER_LAYERS,
+                                max_seq=aw.max_seq, max_tokens=4, rope_theta=aw.theta,
+                                norm_eps=aw.eps)
+    att = moe.AttnLayer(acfg, arena=pool_take(moe.attn_weight_bytes(acfg)),
+                        cache=pool_take(moe.attn_cache_bytes(acfg)),
+                        workspace=pool_take(moe.attn_workspace_bytes(acfg)))
+    staging = staging_buffer(sw)
+    stg = pool_take(aw.d * aw.nqkv * 2).view(torch.int16)
+    stg2 = pool_take(aw.n_heads * aw.hd * aw.d * 2).view(torch.int16)
+    s = ffn.stream
+    t0 = time.perf_counter()
+    for li in range(DECODER_LAYERS):
+        load_layer_device(ffn, sw, li, li, staging)
+        mi.gen_bf16_device(aw.seed, mi.stream_id(mi.KIND_WQKV, li), aw.d * aw.nqkv, aw.sigma_qkv,
+                           stg.data_ptr(), s)
+        mi.gen_bf16_device(aw.seed, mi.stream_id(mi.KIND_WO, li), aw.n_heads * aw.hd * aw.d,
+                           aw.sigma_o, stg2.data_ptr(), s)
+        att.load_layer(li, torch.from_numpy(aw.gamma(li)).cuda(), stg, stg2)
+        K, V = att.cache_views(li)
+        mi.gen_bf16_device(aw.seed, mi.stream_id(mi.KIND_KCACHE, li), K.numel(), aw.sigma_cache,
+                           K.data_ptr(), s)
+        mi.gen_bf16_device(aw.seed, mi.stream_id(mi.KIND_VCACHE, li), V.numel(), aw.sigma_cache,
+                           V.data_ptr(), s)
+    torch.cuda.synchronize()
+    log(f"decoder: {DECODER_LAYERS} layers generated and prestacked in {time.perf_counter() - t0:.1f} s")
+    del staging, stg, stg2
+    x0 = torch.from_numpy(aw.x().view(np.int16)).cuda()
+    pos0 = aw.pos0
+    # touched experts per layer along the chain
+    touched = []
+    x = x0.clone()
+    for li in range(DECODER_LAYERS):
+        att.forward(li, x, x, pos0)
+        rt = ffn.routing_tensors(ffn.route(li, x))
+        touched.append(int((rt["counts"] > 0).sum()))
+        ffn.forward_layers(li, 1, x)
+    torch.cuda.synchronize()
+    out_bits = x.cpu().numpy().view(np.uint16)
+    finite = bool(np.isfinite(mi.bf16_bits_to_f32(out_bits)).all())
+
+    def step():
+        x.copy_(x0)
+        for li in range(DECODER_LAYERS):
+            att.forward(li, x, x, pos0)
+            ffn.forward_layers(li, 1, x)
+
+    for _ in range(warmup):
+        step()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(steps):
+        step()
+    torch.cuda.synchronize()
+    ms_direct = (time.perf_counter() - t0) * 1e3 / steps
+    ms_graph = graph_ms(step, steps, warmup)
+    ms = min(ms_direct, ms_graph)
+    expert_bytes = 3 * sw.d * sw.f * 2
+    attn_b = (aw.d * aw.nqkv * 2 + aw.n_heads * aw.hd * aw.d * 2 + aw.d * 4 +
+              2 * aw.n_kv * (pos0 + 1) * aw.hd * 2)
+    bytes_tok = sum(touched) * expert_bytes + DECODER_LAYERS * (sw.d * sw.E * 4 + attn_b)
+    out = {"workload": "dbrx_decoder_40_layers", "T": 1, "context": pos0 + 1,
+           "n_layers": DECODER_LAYERS,
+           "resident_gb": (DECODER_LAYERS * sw.E * expert_bytes + moe.attn_weight_bytes(acfg)) / 1e9,
+           "ms_per_token": ms, "ms_graph": ms_graph, "ms_direct_launch": ms_direct,
+           "tokens_per_s": 1e3 / ms, "touched_experts_per_layer": touched,
+           "hbm_gb_per_token": bytes_tok / 1e9, "hbm_gbs": bytes_tok / (ms * 1e-3) / 1e9,
+           "hbm_frac": bytes_tok / (ms * 1e-3) / 1e9 / HBM_PEAK_GBS, "output_finite": finite}
+    log(f"decoder: {ms:.2f} ms/token ({1e3 / ms:.1f} tok/s), graph {ms_graph:.2f}, "
+        f"direct {ms_direct:.2f}, {out['hbm_gbs']:.0f} GB/s")
+    ffn.close()
+    att.close()
+    del ffn, att, x, x0
+    return out
+
+
 def gemm_timeline(layer, x):
     """One forward with the per-workgroup GEMM timeline on
     (moe_profile_gemm_timeline), its two GEMMs also event-timed: for each
@@ -722,6 +840,7 @@ def main():
     ap.add_argument("--no-ep-share", action="store_true")
     ap.add_argument("--no-stack", action="store_true")
     ap.add_argument("--no-attn", action="store_true")
+    ap.add_argument("--no-decoder", action="store_true")
     ap.add_argument("--attn-only", action="store_true",
                     help="time only the attention block (for profiling)")
     ap.add_argument("--stack-steps", type=int, default=20)
@@ -765,6 +884,10 @@ def main():
         stack_need = section_bytes(cfg_of(kw0, n_layers=kw0.n_layers, max_tokens=kw0.T), kw0)
         if stack_need + (8 << 30) <= torch.cuda.mem_get_info()[0]:
             sizes.append(stack_need)
+    if not args.no_decoder and not args.prefill_only and not args.attn_only:
+        dec_need = decoder_bytes()
+        if dec_need + (8 << 30) <= torch.cuda.mem_get_info()[0]:
+            sizes.append(dec_need)
     pool_init(max(sizes))
 
     if args.calibrate_copy:
@@ -869,6 +992,11 @@ def main():
         log("setup and timing of the 32-layer stack ...")
         stack = stack_section(args.stack_steps, 3)
 
+    decoder = None
+    if not args.no_decoder:
+        log("setup and timing of the 40-layer decoder ...")
+        decoder = decoder_section(args.stack_steps, 3)
+
     cpu = None
     if not args.no_cpu_baseline:
         log("timing the CPU oracle ...")
@@ -918,6 +1046,7 @@ def main():
         "ep_share": ep_share,
         "attention": attention,
         "stack": stack,
+        "decoder": decoder,
         "perf_model": model,
     }
     pool_release()
