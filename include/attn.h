@@ -45,7 +45,12 @@ typedef struct attn_ctx attn_ctx;
  *                n_heads head_dim a multiple of 256.
  *   n_layers   : layers held in the weight arena and the cache (>= 1).
  *   max_seq    : cache positions per layer (>= 1).
- *   max_tokens : largest T of a call, 1 .. 16 (decode).
+ *   max_tokens : largest T of a call, 1 .. 32768.  Up to 16 tokens a call
+ *                takes the decode path (weight-streaming GEMVs, attention
+ *                over position chunks); above, the prefill path (matrix-core
+ *                GEMMs for the projections, causal attention on the matrix
+ *                cores), which needs (n_heads + 2 n_kv_heads) head_dim to be
+ *                a multiple of 256 when max_tokens > 16.
  *   rope_theta : base of the rotary frequencies (> 1).
  *   norm_eps   : layer-norm epsilon (>= 0).
  *   flags      : must be 0. */
@@ -61,8 +66,9 @@ typedef struct {
  * then Wqkv and Wo repacked into the fragment-tiled layout
  * of moe.h's experts, the query and key rows of Wqkv reordered within each
  * head so that the two members of every rotation pair share a 16-row tile),
- * of the key/value cache, and of the workspace; 0 if
- * cfg is invalid.  Cache layout, per layer l: K then V, each bf16
+ * of the key/value cache, and of the workspace (which, when max_tokens > 16,
+ * also holds a small tile table that attn_init writes); 0 if cfg is
+ * invalid.  Cache layout, per layer l: K then V, each bf16
  * [n_kv_heads][max_seq][head_dim] (head-major, positions contiguous), so K of
  * layer l head g position p starts at element
  * ((l * 2 + 0) * n_kv_heads + g) * max_seq * head_dim + p * head_dim.  A
@@ -73,8 +79,10 @@ MOE_API size_t attn_workspace_bytes(const attn_config *cfg);
 
 /* Sec. 4.1's persistent buffers, applied to the block: validates cfg and
  * records the three caller-allocated device buffers (256-byte aligned, kept
- * until attn_destroy).  Allocates only the host-side context.  Errors as
- * moe_init; the message is readable through attn_last_error(NULL). */
+ * until attn_destroy).  Allocates only the host-side context; when
+ * max_tokens > 16 it also copies the prefill tile table into the workspace
+ * (a synchronous copy; MOE_E_HIP if it fails).  Errors as moe_init; the
+ * message is readable through attn_last_error(NULL). */
 MOE_API moe_status attn_init(const attn_config *cfg, void *weight_arena, void *kv_cache,
                              void *workspace, attn_ctx **out);
 
@@ -109,12 +117,14 @@ MOE_API moe_status attn_intermediates(const attn_ctx *ctx, const uint16_t **h, c
  * kinds of attn_kernel_kind. */
 typedef enum {
     ATTN_K_NORM = 0,       /* layer norm */
-    ATTN_K_QKV = 1,        /* fused projection + rotary + cache append */
-    ATTN_K_SCORE = 2,      /* attention over position chunks */
-    ATTN_K_COMBINE = 3,    /* merge of the chunks */
-    ATTN_K_OUT = 4,        /* output projection + residual */
+    ATTN_K_QKV = 1,        /* fused projection (+ rotary + cache append in decode) */
+    ATTN_K_SCORE = 2,      /* attention (over position chunks in decode, causal in prefill) */
+    ATTN_K_COMBINE = 3,    /* merge of the chunks (decode) */
+    ATTN_K_OUT = 4,        /* output projection (+ residual in decode) */
     ATTN_K_PACK = 5,       /* weight repacking */
-    ATTN_K_COUNT = 6
+    ATTN_K_ROPE = 6,       /* rotary + cache append (prefill) */
+    ATTN_K_RESIDUAL = 7,   /* y = bf16(x + o) (prefill) */
+    ATTN_K_COUNT = 8
 } attn_kernel_kind;
 MOE_API moe_status attn_profile_enable(attn_ctx *ctx, int32_t max_launches);
 MOE_API moe_status attn_profile_read(attn_ctx *ctx, double *total_ms, int64_t *launches,

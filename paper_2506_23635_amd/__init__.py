@@ -35,7 +35,7 @@ EXPORTED = ["moe_weight_bytes", "moe_workspace_bytes", "moe_workspace_map", "moe
             "attn_load_layer", "attn_forward", "attn_intermediates", "attn_profile_enable",
             "attn_profile_read", "attn_destroy", "attn_last_error"]
 
-ATTN_KERNEL_KINDS = ["norm", "qkv", "score", "combine", "out", "pack"]
+ATTN_KERNEL_KINDS = ["norm", "qkv", "score", "combine", "out", "pack", "rope", "residual"]
 
 KERNEL_KINDS = ["router", "route", "decode_gateup", "decode_down", "gemm_gateup", "gemm_down",
                 "combine", "pack"]

@@ -16,6 +16,11 @@
 //   combine_kernel  merges the chunks of each (token, head) into bf16 a
 //   gemv_kernel     o = a Wo (fp32) and y = bf16(x + o)
 //
+// Above 16 new tokens (prefill) the block is: norm_kernel -> q|k|v on the
+// grouped GEMM of moe_prefill.hip -> rope_kernel (rotation, cache append)
+// -> flash_kernel (causal attention on the matrix cores) -> o = a Wo on the
+// grouped GEMM -> residual_kernel.
+//
 // The GEMVs stream the fragment-tiled weights (the layout of moe_common.h)
 // through v_mfma_f32_16x16x32_bf16 with the tokens as the B operand, as the
 // MoE decode GEMVs do: one workgroup per 16 output features, its 8 waves
@@ -44,6 +49,9 @@ __device__ inline u32x4_t ld16_nt(const void* p)
 }
 
 __device__ inline u32x4_t ld16(const void* p) { return *reinterpret_cast<const u32x4_t*>(p); }
+
+// the fp32 value of bf16(v) (round to nearest even)
+__device__ inline float bf16_round(float v) { return __uint_as_float((uint32_t)moe::f32_to_bf16(v) << 16); }
 
 // The output projection, o = a Wo (fp32) and y = bf16(x + o), one
 // workgroup per 16 output features.
@@ -636,6 +644,240 @@ __global__ __launch_bounds__(128) void combine_kernel(CombineArgs a)
     a.out[(int64_t)th * a.hd + i] = moe::f32_to_bf16(acc / L);
 }
 
+// ---------------------------------------------------------------- prefill
+// More than 16 new tokens: the projections run on the grouped GEMM of
+// moe_prefill.hip (one "expert", its rows the tokens), then these kernels.
+
+// rope_kernel, one workgroup per token: from the projection's fp32 output
+// in packed row order (query and key features placed by rope_row), the
+// natural-order fp32 q|k|v (kept for inspection), q rotated to bf16 in the
+// workspace, k rotated and v to the cache at position pos0 + t.  The angle
+// and rotation arithmetic are the decode epilogue's (rope_cs).
+struct RopeArgs {
+    const float* qkvp;     // [T][nqkv] fp32, packed row order
+    const double* inv_freq;
+    float* qkv;            // [T][nqkv] fp32, natural order
+    uint16_t* q;           // [T][H][hd]
+    uint16_t* kc;
+    uint16_t* vc;
+    int T, H, G, hd, max_seq, pos0;
+};
+
+__global__ __launch_bounds__(256) void rope_kernel(RopeArgs a)
+{
+    const int t = blockIdx.x;
+    const int hd = a.hd, half = hd / 2;
+    const int nqk = (a.H + a.G) * hd, nqkv = nqk + a.G * hd;
+    const int pos = a.pos0 + t;
+    const float* src = a.qkvp + (int64_t)t * nqkv;
+    float* nat = a.qkv + (int64_t)t * nqkv;
+    for (int e = threadIdx.x; e < (a.H + a.G) * half; e += blockDim.x) {
+        const int head = e / half, f = e % half;
+        const int n0 = head * hd + f, n1 = n0 + half;
+        const float x0 = src[moe::rope_row(n0, hd)], x1 = src[moe::rope_row(n1, hd)];
+        nat[n0] = x0;
+        nat[n1] = x1;
+        float c, sf;
+        rope_cs(pos, a.inv_freq[f], c, sf);
+        const float r0 = x0 * c - x1 * sf, r1 = x1 * c + x0 * sf;
+        uint16_t* dst = head < a.H ? a.q + ((int64_t)t * a.H + head) * hd
+                                   : a.kc + ((int64_t)(head - a.H) * a.max_seq + pos) * hd;
+        dst[f] = moe::f32_to_bf16(r0);
+        dst[f + half] = moe::f32_to_bf16(r1);
+    }
+    for (int e = threadIdx.x; e < a.G * hd; e += blockDim.x) {
+        const float v = src[nqk + e];
+        nat[nqk + e] = v;
+        a.vc[((int64_t)(e / hd) * a.max_seq + pos) * hd + e % hd] = moe::f32_to_bf16(v);
+    }
+}
+
+// flash_kernel: causal attention of T new tokens, one workgroup of 4 waves
+// per (query head j, block of 64 query tokens); wave w owns tokens
+// 16 w .. 16 w + 15 of the block, one per lane column.  Per step of 64
+// positions of head j's key/value head: K rows and V transposed (dims major)
+// go to LDS; the scores are computed transposed, S^T = K Q^T, with
+// v_mfma_f32_16x16x32_bf16 (A = 16 positions x 32 dims of K from LDS, B =
+// the wave's query rows), so lane l ends with the scores of token l%16 at
+// positions 4(l/16) + r of each 16-position block; the running maximum and
+// sum per token (two butterfly steps) rescale the output, and O^T += V^T P^T
+// takes the P values straight from those registers as the B operand (the
+// 8 positions of a lane's K group are {4g..4g+3, 16+4g..16+4g+3} of a
+// 32-position block, and the V^T operand is read from LDS in the same
+// order).  P enters the matrix cores as two bf16 terms, bf16(p) and
+// bf16(p - bf16(p)), which keep 16 significant bits; V is bf16 and every
+// product is exact in the fp32 accumulation.
+struct FlashArgs {
+    const uint16_t* q;     // [T][H][HD] bf16, rotated
+    const uint16_t* kc;    // this layer's K cache [G][max_seq][HD]
+    const uint16_t* vc;
+    uint16_t* out;         // a [T][H * HD] bf16
+    int T, H, G, max_seq, pos0;
+    float scale;
+};
+
+constexpr int kFlashQ = 64;     // query tokens per workgroup
+constexpr int kFlashP = 64;     // positions per step
+
+__device__ inline uint32_t pack_bf16x2(float lo, float hi)
+{
+    return (uint32_t)moe::f32_to_bf16(lo) | ((uint32_t)moe::f32_to_bf16(hi) << 16);
+}
+
+template <int HD>
+__global__ __launch_bounds__(256) void flash_kernel(FlashArgs a)
+{
+    constexpr int KS = HD / 32;              // K steps of the score MFMAs
+    constexpr int DB = HD / 16;              // 16-dim blocks of the output
+    constexpr int KROW = HD + 8;             // padded K row in LDS (bf16)
+    constexpr int VROW = kFlashP + 8;        // padded V^T row (positions, bf16)
+    __shared__ __attribute__((aligned(16))) uint16_t ks[kFlashP * KROW];
+    __shared__ __attribute__((aligned(16))) uint16_t vt[HD * VROW];
+    const int j = blockIdx.x, qb = blockIdx.y;
+    const int kvh = j / (a.H / a.G);
+    const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+    const int c = lane & 15, grp = lane >> 4;
+    const int t = qb * kFlashQ + w * 16 + c;            // this lane's token
+    const bool tok_ok = t < a.T;
+    const int lim = a.pos0 + t;                          // its last position
+    const u32x4_t zero = {0u, 0u, 0u, 0u};
+    u32x4_t qf[KS];
+    {
+        const uint16_t* qrow = a.q + ((int64_t)(tok_ok ? t : 0) * a.H + j) * HD + grp * 8;
+#pragma unroll
+        for (int k = 0; k < KS; ++k) {
+            const u32x4_t v = ld16(qrow + k * 32);
+            qf[k] = tok_ok ? v : zero;
+        }
+    }
+    f32x4_t o[DB];
+#pragma unroll
+    for (int b = 0; b < DB; ++b) o[b] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+    float m = -INFINITY, l = 0.f;
+    const int t_last = min(qb * kFlashQ + kFlashQ, a.T) - 1;
+    const int n_pos = a.pos0 + t_last + 1;               // positions the block needs
+    const uint16_t* kbase = a.kc + (int64_t)kvh * a.max_seq * HD;
+    const uint16_t* vbase = a.vc + (int64_t)kvh * a.max_seq * HD;
+    uint32_t* vt32 = reinterpret_cast<uint32_t*>(vt);
+    for (int p0 = 0; p0 < n_pos; p0 += kFlashP) {
+        const int live = min(kFlashP, n_pos - p0);
+        __syncthreads();                                 // the last step's LDS reads are done
+        // K rows: 16-byte pieces, coalesced
+        for (int e = threadIdx.x; e < kFlashP * (HD / 8); e += 256) {
+            const int p = e / (HD / 8), k8 = e % (HD / 8);
+            const u32x4_t v = ld16(kbase + (int64_t)(p0 + min(p, live - 1)) * HD + k8 * 8);
+            *reinterpret_cast<u32x4_t*>(&ks[p * KROW + k8 * 8]) = p < live ? v : zero;
+        }
+        // V transposed: a thread takes positions 2 pp, 2 pp + 1 at 8 dims and
+        // writes 8 words of (position pair) per dim
+        for (int e = threadIdx.x; e < (kFlashP / 2) * (HD / 8); e += 256) {
+            const int pp = e % (kFlashP / 2), k8 = e / (kFlashP / 2);
+            const int pa = 2 * pp, pb = 2 * pp + 1;
+            const u32x4_t va = ld16(vbase + (int64_t)(p0 + min(pa, live - 1)) * HD + k8 * 8);
+            const u32x4_t vb = ld16(vbase + (int64_t)(p0 + min(pb, live - 1)) * HD + k8 * 8);
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                const uint32_t a0 = pa < live ? va[i] : 0u, b0 = pb < live ? vb[i] : 0u;
+                vt32[((k8 * 8 + 2 * i) * VROW) / 2 + pp] = (a0 & 0xFFFFu) | (b0 << 16);
+                vt32[((k8 * 8 + 2 * i + 1) * VROW) / 2 + pp] = (a0 >> 16) | (b0 & 0xFFFF0000u);
+            }
+        }
+        __syncthreads();
+        // S^T for the 4 blocks of 16 positions
+        f32x4_t st[4];
+#pragma unroll
+        for (int pb = 0; pb < 4; ++pb) {
+            st[pb] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+            for (int k = 0; k < KS; ++k) {
+                const u32x4_t kf =
+                    *reinterpret_cast<const u32x4_t*>(&ks[(pb * 16 + c) * KROW + k * 32 + grp * 8]);
+                st[pb] = moe::mfma16x16x32(kf, qf[k], st[pb]);
+            }
+        }
+        // scale, causal mask, running maximum and sum of token c
+        float sv[16];
+        float mx = -INFINITY;
+#pragma unroll
+        for (int pb = 0; pb < 4; ++pb)
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+                const int pos = p0 + pb * 16 + 4 * grp + r;
+                const float v = (tok_ok && pos <= lim) ? st[pb][r] * a.scale : -INFINITY;
+                sv[pb * 4 + r] = v;
+                mx = fmaxf(mx, v);
+            }
+        mx = fmaxf(mx, __shfl_xor(mx, 16, 64));
+        mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
+        const float mn = fmaxf(m, mx);
+        const float alpha = m == -INFINITY ? 0.f : expf(m - mn);
+        float ps = 0.f;
+        float pv[16];
+#pragma unroll
+        for (int e = 0; e < 16; ++e) {
+            pv[e] = sv[e] == -INFINITY ? 0.f : expf(sv[e] - mn);
+            ps += pv[e];
+        }
+        ps += __shfl_xor(ps, 16, 64);
+        ps += __shfl_xor(ps, 32, 64);
+        l = l * alpha + ps;
+        m = mn;
+#pragma unroll
+        for (int b = 0; b < DB; ++b) o[b] *= alpha;
+        // O^T += V^T P^T over the two 32-position K blocks, P as hi + lo
+#pragma unroll
+        for (int kb = 0; kb < 2; ++kb) {
+            u32x4_t bh, bl;
+#pragma unroll
+            for (int i = 0; i < 2; ++i) {
+                const float* pq = &pv[(2 * kb + i) * 4];
+                const float h0 = bf16_round(pq[0]), h1 = bf16_round(pq[1]);
+                const float h2 = bf16_round(pq[2]), h3 = bf16_round(pq[3]);
+                bh[2 * i] = pack_bf16x2(h0, h1);
+                bh[2 * i + 1] = pack_bf16x2(h2, h3);
+                bl[2 * i] = pack_bf16x2(pq[0] - h0, pq[1] - h1);
+                bl[2 * i + 1] = pack_bf16x2(pq[2] - h2, pq[3] - h3);
+            }
+#pragma unroll
+            for (int b = 0; b < DB; ++b) {
+                const uint32_t* vr = vt32 + ((b * 16 + c) * VROW + kb * 32 + 4 * grp) / 2;
+                const uint2 v0 = *reinterpret_cast<const uint2*>(vr);
+                const uint2 v1 = *reinterpret_cast<const uint2*>(vr + 8);
+                const u32x4_t av = {v0.x, v0.y, v1.x, v1.y};
+                o[b] = moe::mfma16x16x32(av, bh, o[b]);
+                o[b] = moe::mfma16x16x32(av, bl, o[b]);
+            }
+        }
+    }
+    if (!tok_ok) return;
+    // lane: dims 16 b + 4 grp + r of token t
+    const float inv = 1.0f / l;
+    uint16_t* dst = a.out + ((int64_t)t * a.H + j) * HD + 4 * grp;
+#pragma unroll
+    for (int b = 0; b < DB; ++b)
+        *reinterpret_cast<uint2*>(dst + b * 16) =
+            make_uint2(pack_bf16x2(o[b][0] * inv, o[b][1] * inv), pack_bf16x2(o[b][2] * inv, o[b][3] * inv));
+}
+
+// y = bf16(x + o), 8 elements per thread
+__global__ __launch_bounds__(256) void residual_kernel(const uint16_t* __restrict__ x,
+                                                       const float* __restrict__ o,
+                                                       uint16_t* y, int64_t n8)
+{
+    const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (i >= n8) return;
+    const u32x4_t xv = ld16(x + i * 8);
+    const float4 o0 = *reinterpret_cast<const float4*>(o + i * 8);
+    const float4 o1 = *reinterpret_cast<const float4*>(o + i * 8 + 4);
+    const float ov[8] = {o0.x, o0.y, o0.z, o0.w, o1.x, o1.y, o1.z, o1.w};
+    u32x4_t out;
+#pragma unroll
+    for (int k = 0; k < 4; ++k)
+        out[k] = pack_bf16x2(__uint_as_float(xv[k] << 16) + ov[2 * k],
+                             __uint_as_float(xv[k] & 0xFFFF0000u) + ov[2 * k + 1]);
+    *reinterpret_cast<u32x4_t*>(y + i * 8) = out;
+}
+
 }  // namespace attn
 
 extern "C" {
@@ -690,6 +932,37 @@ hipError_t attn_launch_score(const uint16_t* q, const uint16_t* kc, const uint16
         hipLaunchKernelGGL(attn::score_kernel<128>, dim3(G, n_chunks), dim3(256), 0, s, a);
     else
         hipLaunchKernelGGL(attn::score_kernel<64>, dim3(G, n_chunks), dim3(256), 0, s, a);
+    return hipGetLastError();
+}
+
+hipError_t attn_launch_rope(const float* qkvp, const double* inv_freq, float* qkv, uint16_t* q,
+                            uint16_t* kc, uint16_t* vc, int T, int H, int G, int hd, int max_seq,
+                            int pos0, hipStream_t s)
+{
+    attn::RopeArgs a{qkvp, inv_freq, qkv, q, kc, vc, T, H, G, hd, max_seq, pos0};
+    hipLaunchKernelGGL(attn::rope_kernel, dim3(T), dim3(256), 0, s, a);
+    return hipGetLastError();
+}
+
+hipError_t attn_launch_flash(const uint16_t* q, const uint16_t* kc, const uint16_t* vc,
+                             uint16_t* out, int T, int H, int G, int hd, int max_seq, int pos0,
+                             hipStream_t s)
+{
+    attn::FlashArgs a{q, kc, vc, out, T, H, G, max_seq, pos0, (float)(1.0 / sqrt((double)hd))};
+    const dim3 grid(H, (T + attn::kFlashQ - 1) / attn::kFlashQ);
+    if (hd == 128)
+        hipLaunchKernelGGL(attn::flash_kernel<128>, grid, dim3(256), 0, s, a);
+    else
+        hipLaunchKernelGGL(attn::flash_kernel<64>, grid, dim3(256), 0, s, a);
+    return hipGetLastError();
+}
+
+hipError_t attn_launch_residual(const uint16_t* x, const float* o, uint16_t* y, int64_t n,
+                                hipStream_t s)
+{
+    const int64_t n8 = n / 8;
+    hipLaunchKernelGGL(attn::residual_kernel, dim3((unsigned)((n8 + 255) / 256)), dim3(256), 0, s,
+                       x, o, y, n8);
     return hipGetLastError();
 }
 

@@ -1,12 +1,15 @@
 // attn_capi.cpp -- the C-ABI of include/attn.h: configuration checks, the
 // carve-up of the caller's weight arena, cache and workspace, the one-time
 // weight repack (the query and key heads of Wqkv with their rotation pairs
-// in one tile), and the launch sequence of the block (norm, inside the
-// projection up to 4 tokens -> fused projection + rotary + cache append ->
-// attention over position chunks -> merge -> output projection + residual).  Nothing here allocates device
-// memory.
+// in one tile), and the launch sequences of the block: up to 16 tokens
+// (decode) norm, inside the projection up to 4 tokens -> fused projection +
+// rotary + cache append -> attention over position chunks -> merge ->
+// output projection + residual; above 16 (prefill) norm -> projection GEMM
+// -> rotary + cache append -> causal attention -> output GEMM -> residual.
+// Nothing here allocates device memory.
 #include <hip/hip_runtime.h>
 
+#include <algorithm>
 #include <cmath>
 #include <cstring>
 #include <cstdint>
@@ -20,7 +23,8 @@
 namespace {
 
 constexpr size_t kAlign = 256;
-constexpr int kMaxTokens = 16;     // token columns of one MFMA B operand
+constexpr int kDecodeTokens = 16;  // up to here the decode path (token columns of one MFMA B operand)
+constexpr int kMaxTokens = 32768;  // the prefill path's bound (activation buffers below 2^31 bytes)
 constexpr int kMaxGroup = 8;       // query heads per key/value head (attention LDS rows)
 
 size_t align_up(size_t v, size_t a) { return (v + a - 1) / a * a; }
@@ -28,8 +32,8 @@ size_t align_up(size_t v, size_t a) { return (v + a - 1) / a * a; }
 struct Layout {
     size_t gamma_bytes, freq_off, wqkv_off, wqkv_bytes, wo_off, wo_bytes, layer_bytes, arena_bytes;
     size_t cache_head_elems, cache_layer_bytes, cache_bytes;
-    size_t h_off, qkv_off, q_off, part_off, a_off, o_off, ws_bytes;
-    int nqkv, nq, n_chunks;
+    size_t h_off, qkv_off, q_off, part_off, a_off, o_off, qkvp_off, plan_off, ws_bytes;
+    int nqkv, nq, n_chunks, max_tiles;
 };
 
 const char* check_config(const attn_config* c)
@@ -47,7 +51,9 @@ const char* check_config(const attn_config* c)
     if ((int64_t)c->n_heads * c->head_dim > 65536) return "n_heads * head_dim too large";
     if (c->n_layers < 1 || c->n_layers > 1024) return "n_layers must be in [1, 1024]";
     if (c->max_seq < 1 || c->max_seq > (1 << 20)) return "max_seq must be in [1, 2^20]";
-    if (c->max_tokens < 1 || c->max_tokens > kMaxTokens) return "max_tokens must be in [1, 16]";
+    if (c->max_tokens < 1 || c->max_tokens > kMaxTokens) return "max_tokens must be in [1, 32768]";
+    if (c->max_tokens > kDecodeTokens && (int64_t)(c->n_heads + 2 * c->n_kv_heads) * c->head_dim % 256)
+        return "above 16 tokens (n_heads + 2 n_kv_heads) * head_dim must be a multiple of 256";
     if (!(c->rope_theta > 1.0f) || !std::isfinite(c->rope_theta)) return "rope_theta must be > 1";
     if (!(c->norm_eps >= 0.0f) || !std::isfinite(c->norm_eps)) return "norm_eps must be >= 0";
     if (c->flags != 0) return "flags must be 0";
@@ -73,14 +79,23 @@ Layout make_layout(const attn_config* c)
     L.cache_bytes = L.cache_layer_bytes * c->n_layers;
     L.n_chunks = attn_chunks(c->max_seq);
     const size_t Tm = c->max_tokens;
+    const size_t Td = std::min<size_t>(Tm, kDecodeTokens);
+    const int tile_rows = moe_prefill_tile_rows();
+    L.max_tiles = (int)((Tm + tile_rows - 1) / tile_rows);
     size_t off = 0;
     auto take = [&](size_t bytes) { size_t o = off; off = align_up(off + bytes, kAlign); return o; };
     L.h_off = take(Tm * d * 2);
     L.qkv_off = take(Tm * L.nqkv * 4);
     L.q_off = take(Tm * L.nq * 2);
-    L.part_off = take(Tm * H * L.n_chunks * attn_part_stride((int)hd) * 4);
+    L.part_off = take(Td * H * L.n_chunks * attn_part_stride((int)hd) * 4);
     L.a_off = take(Tm * L.nq * 2);
     L.o_off = take(Tm * d * 4);
+    if (Tm > (size_t)kDecodeTokens) {
+        L.qkvp_off = take(Tm * L.nqkv * 4);
+        // the projection GEMMs' tile table: (0, 256 i) per token tile, then
+        // per T: offsets {0, T} and the tile count
+        L.plan_off = take((size_t)L.max_tiles * 8 + (Tm + 1) * 16);
+    }
     L.ws_bytes = off;
     return L;
 }
@@ -147,6 +162,72 @@ uint16_t* layer_v(attn_ctx* c, int l)
     return layer_k(c, l) + (size_t)c->cfg.n_kv_heads * c->L.cache_head_elems;
 }
 
+// One plain GEMM out = in W^T on the grouped GEMM's down mode: a single
+// "expert" whose rows are the T tokens, its weight the packed N x K matrix.
+hipError_t project(attn_ctx* c, const uint8_t* wpk, const uint16_t* in, int K, int N, float* out,
+                   int T, hipStream_t s)
+{
+    const Layout& L = c->L;
+    int32_t* plan = reinterpret_cast<int32_t*>(c->ws + L.plan_off);
+    moe::GemmArgs g{};
+    g.experts = wpk;
+    g.expert_bytes = (uint64_t)N * K * 2;
+    g.gu_bytes = 0;
+    g.H = const_cast<uint16_t*>(in);
+    g.O = out;
+    g.tiles = plan;
+    g.offsets = plan + (size_t)L.max_tiles * 2 + (size_t)T * 4;
+    g.n_tiles = g.offsets + 2;
+    g.d = N;
+    g.f = K;
+    g.e_begin = 0;
+    g.max_tiles = (T + moe_prefill_tile_rows() - 1) / moe_prefill_tile_rows();
+    g.T = T;
+    return moe_launch_gemm_down(&g, s);
+}
+
+// The block for T > 16 new tokens: norm -> q|k|v (GEMM) -> rotation and
+// cache append -> causal attention -> o = a Wo (GEMM) -> residual.
+moe_status prefill(attn_ctx* ctx, int layer, const uint16_t* x, uint16_t* y, int T, int pos0,
+                   hipStream_t s)
+{
+    const attn_config& c = ctx->cfg;
+    const Layout& L = ctx->L;
+    uint8_t* w = layer_w(ctx, layer);
+    uint16_t* h = reinterpret_cast<uint16_t*>(ctx->ws + L.h_off);
+    float* qkv = reinterpret_cast<float*>(ctx->ws + L.qkv_off);
+    float* qkvp = reinterpret_cast<float*>(ctx->ws + L.qkvp_off);
+    uint16_t* q = reinterpret_cast<uint16_t*>(ctx->ws + L.q_off);
+    uint16_t* a = reinterpret_cast<uint16_t*>(ctx->ws + L.a_off);
+    float* o = reinterpret_cast<float*>(ctx->ws + L.o_off);
+    const int d = c.d_model;
+    const float* gamma = reinterpret_cast<const float*>(w);
+    hipError_t e = timed(ctx, ATTN_K_NORM, s, [&] {
+        return attn_launch_norm(x, gamma, T, d, c.norm_eps, h, s);
+    });
+    if (e != hipSuccess) return hip_fail(ctx, e, "norm kernel launch");
+    e = timed(ctx, ATTN_K_QKV, s, [&] { return project(ctx, w + L.wqkv_off, h, d, L.nqkv, qkvp, T, s); });
+    if (e != hipSuccess) return hip_fail(ctx, e, "projection GEMM launch");
+    e = timed(ctx, ATTN_K_ROPE, s, [&] {
+        return attn_launch_rope(qkvp, reinterpret_cast<const double*>(w + L.freq_off), qkv, q,
+                                layer_k(ctx, layer), layer_v(ctx, layer), T, c.n_heads,
+                                c.n_kv_heads, c.head_dim, c.max_seq, pos0, s);
+    });
+    if (e != hipSuccess) return hip_fail(ctx, e, "rotation kernel launch");
+    e = timed(ctx, ATTN_K_SCORE, s, [&] {
+        return attn_launch_flash(q, layer_k(ctx, layer), layer_v(ctx, layer), a, T, c.n_heads,
+                                 c.n_kv_heads, c.head_dim, c.max_seq, pos0, s);
+    });
+    if (e != hipSuccess) return hip_fail(ctx, e, "attention kernel launch");
+    e = timed(ctx, ATTN_K_OUT, s, [&] { return project(ctx, w + L.wo_off, a, L.nq, d, o, T, s); });
+    if (e != hipSuccess) return hip_fail(ctx, e, "output projection GEMM launch");
+    e = timed(ctx, ATTN_K_RESIDUAL, s, [&] {
+        return attn_launch_residual(x, o, y, (int64_t)T * d, s);
+    });
+    if (e != hipSuccess) return hip_fail(ctx, e, "residual kernel launch");
+    return MOE_OK;
+}
+
 }  // namespace
 
 extern "C" {
@@ -183,6 +264,23 @@ moe_status attn_init(const attn_config* cfg, void* weight_arena, void* kv_cache,
     c->arena = static_cast<uint8_t*>(weight_arena);
     c->cache = static_cast<uint8_t*>(kv_cache);
     c->ws = static_cast<uint8_t*>(workspace);
+    if (cfg->max_tokens > kDecodeTokens) {
+        // the prefill projections' tile table, written once into the workspace
+        const int tile_rows = moe_prefill_tile_rows();
+        std::vector<int32_t> plan((size_t)c->L.max_tiles * 2 + ((size_t)cfg->max_tokens + 1) * 4, 0);
+        for (int i = 0; i < c->L.max_tiles; ++i) plan[2 * i + 1] = i * tile_rows;
+        for (int T = 0; T <= cfg->max_tokens; ++T) {
+            int32_t* e = &plan[(size_t)c->L.max_tiles * 2 + (size_t)T * 4];
+            e[1] = T;
+            e[2] = (T + tile_rows - 1) / tile_rows;
+        }
+        const hipError_t e = hipMemcpy(c->ws + c->L.plan_off, plan.data(), plan.size() * 4,
+                                       hipMemcpyHostToDevice);
+        if (e != hipSuccess) {
+            delete c;
+            return fail(nullptr, MOE_E_HIP, std::string("tile table copy: ") + hipGetErrorString(e));
+        }
+    }
     c->loaded.assign(cfg->n_layers, 0);
     c->prof_on = false;
     c->prof_dropped = 0;
@@ -269,6 +367,7 @@ moe_status attn_forward(attn_ctx* ctx, int32_t layer, const uint16_t* x, uint16_
     const int d = c.d_model;
     const float* gamma = reinterpret_cast<const float*>(w);
     hipError_t e = hipSuccess;
+    if (T > kDecodeTokens) return prefill(ctx, layer, x, y, T, pos0, s);
     if (!attn_norm_in_projection(T)) {
         e = timed(ctx, ATTN_K_NORM, s, [&] {
             return attn_launch_norm(x, gamma, T, d, c.norm_eps, h, s);

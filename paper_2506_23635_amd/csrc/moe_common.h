@@ -169,6 +169,14 @@ hipError_t attn_launch_qkv(const void* w, uint16_t* h, const uint16_t* x, const 
                            int max_seq, int pos0, hipStream_t s);
 hipError_t attn_launch_out(const void* w, const uint16_t* x, int T, int K, int N, float* y32,
                            const uint16_t* res, uint16_t* y16, hipStream_t s);
+hipError_t attn_launch_rope(const float* qkvp, const double* inv_freq, float* qkv, uint16_t* q,
+                            uint16_t* kc, uint16_t* vc, int T, int H, int G, int hd, int max_seq,
+                            int pos0, hipStream_t s);
+hipError_t attn_launch_flash(const uint16_t* q, const uint16_t* kc, const uint16_t* vc,
+                             uint16_t* out, int T, int H, int G, int hd, int max_seq, int pos0,
+                             hipStream_t s);
+hipError_t attn_launch_residual(const uint16_t* x, const float* o, uint16_t* y, int64_t n,
+                                hipStream_t s);
 int attn_chunks(int n_pos);
 int attn_part_stride(int hd);
 hipError_t attn_launch_score(const uint16_t* q, const uint16_t* kc, const uint16_t* vc,

@@ -257,14 +257,17 @@ def test_attn_sizes():
 
 
 @pytest.mark.parametrize("bad", [dict(d_model=200), dict(d_model=8448), dict(head_dim=96), dict(n_kv_heads=5),
-                                 dict(n_heads=64, n_kv_heads=4), dict(max_tokens=17),
+                                 dict(n_heads=64, n_kv_heads=4), dict(max_tokens=32769),
+                                 dict(n_heads=4, n_kv_heads=1, head_dim=64, max_tokens=17),
                                  dict(max_tokens=0), dict(max_seq=0), dict(n_layers=0),
                                  dict(rope_theta=1.0), dict(norm_eps=-1.0), dict(flags=1),
                                  dict(n_heads=3, n_kv_heads=1, head_dim=64)])
 def test_attn_bad_configs_rejected(bad):
     # n_heads 64 over 4 key/value heads: 16 query heads share one, past the
     # attention kernel's 8; 3 heads of 64: the output projection's K (192) is
-    # not a multiple of 256
+    # not a multiple of 256; 4 + 2 heads of 64 (384 fused rows) cannot take
+    # the prefill GEMM's 256-row tiles, so such a config is limited to 16
+    # tokens
     cfg = _attn_cfg(**bad)
     assert moe.attn_weight_bytes(cfg) == 0
     out = ctypes.c_void_p()
