@@ -386,6 +386,7 @@ def stack_section(steps, warmup):
 
 
 DECODER_LAYERS = 40     # DBRX's layer count (Table tab:vars)
+DECODER_PROMPT = 2048   # the long-prompt workload's prompt (2000 tokens), rounded
 
 
 def decoder_bytes():
@@ -396,20 +397,22 @@ def decoder_bytes():
     import paper_2506_23635_amd as moe
     sw = mi.WORKLOADS["stack"].with_(n_layers=DECODER_LAYERS, T=1)
     aw = mi.ATTN_WORKLOADS["attn_decode"]
-    mcfg = moe.make_config(sw.d, sw.f, sw.E, sw.k, n_layers=DECODER_LAYERS, max_tokens=4)
+    mcfg = moe.make_config(sw.d, sw.f, sw.E, sw.k, n_layers=DECODER_LAYERS,
+                           max_tokens=DECODER_PROMPT)
     acfg = moe.make_attn_config(aw.d, aw.n_heads, aw.n_kv, aw.hd, n_layers=DECODER_LAYERS,
-                                max_seq=aw.max_seq, max_tokens=4, rope_theta=aw.theta,
-                                norm_eps=aw.eps)
-    return (section_bytes(mcfg, sw) + moe.attn_weight_bytes(acfg) + moe.attn_cache_bytes(acfg) +
+                                max_seq=aw.max_seq, max_tokens=DECODER_PROMPT,
+                                rope_theta=aw.theta, norm_eps=aw.eps)
+    return (section_bytes(mcfg, sw) + 2 * DECODER_PROMPT * aw.d * 2 + moe.attn_weight_bytes(acfg) + moe.attn_cache_bytes(acfg) +
             moe.attn_workspace_bytes(acfg) + (aw.d * aw.nqkv + aw.n_heads * aw.hd * aw.d) * 2 +
             (64 << 20))
 
 
 def decoder_section(steps, warmup):
-    """A whole DBRX-shaped decoder on one GPU: 40 layers, each the
-    self-attention block (one token after 2047 cached positions) and then
-    the 16-expert MoE layer with its residual (moe_forward_layers), every
-    weight resident (254 GB of experts + 7 GB of attention).  One step is
+    """A whole DBRX-shaped decoder on one GPU: 40 layers, each as DBRX
+    arranges it -- norm, self-attention (one token after 2047 cached
+    positions) and residual, norm, the 16-expert MoE layer and residual
+    (attn_forward_norm, moe_forward_residual) -- every weight resident
+    (254 GB of experts + 7 GB of attention).  One step is
     one generated token through all 40 layers; timed with direct launches
     and as HIP graph replays of the whole step.  HBM bytes per token: the
     touched experts (4 per layer at T = 1), the routers, and each layer's
@@ -426,11 +429,12 @@ def decoder_section(steps, warmup):
         log(f"decoder: skipped ({have / 1e9:.0f} GB of pool, {need / 1e9:.0f} GB needed)")
         return None
     pool_reset()
-    mcfg = moe.make_config(sw.d, sw.f, sw.E, sw.k, n_layers=DECODER_LAYERS, max_tokens=4)
+    mcfg = moe.make_config(sw.d, sw.f, sw.E, sw.k, n_layers=DECODER_LAYERS,
+                           max_tokens=DECODER_PROMPT)
     ffn = pool_layer(mcfg)
     acfg = moe.make_attn_config(aw.d, aw.n_heads, aw.n_kv, aw.hd, n_layers=DECODER_LAYERS,
-                                max_seq=aw.max_seq, max_tokens=4, rope_theta=aw.theta,
-                                norm_eps=aw.eps)
+                                max_seq=aw.max_seq, max_tokens=DECODER_PROMPT,
+                                rope_theta=aw.theta, norm_eps=aw.eps)
     att = moe.AttnLayer(acfg, arena=pool_take(moe.attn_weight_bytes(acfg)),
                         cache=pool_take(moe.attn_cache_bytes(acfg)),
                         workspace=pool_take(moe.attn_workspace_bytes(acfg)))
@@ -446,6 +450,7 @@ def decoder_section(steps, warmup):
         mi.gen_bf16_device(aw.seed, mi.stream_id(mi.KIND_WO, li), aw.n_heads * aw.hd * aw.d,
                            aw.sigma_o, stg2.data_ptr(), s)
         att.load_layer(li, torch.from_numpy(aw.gamma(li)).cuda(), stg, stg2)
+        att.load_post_norm(li, torch.from_numpy(aw.gamma2(li)).cuda())
         K, V = att.cache_views(li)
         mi.gen_bf16_device(aw.seed, mi.stream_id(mi.KIND_KCACHE, li), K.numel(), aw.sigma_cache,
                            K.data_ptr(), s)
@@ -456,14 +461,16 @@ def decoder_section(steps, warmup):
     del staging, stg, stg2
     x0 = torch.from_numpy(aw.x().view(np.int16)).cuda()
     pos0 = aw.pos0
-    # touched experts per layer along the chain
+    # touched experts per layer along the chain; a layer is DBRX's: y =
+    # x + attention(norm1(x)), z = norm2(y), x = y + moe(z)
     touched = []
     x = x0.clone()
+    z = torch.empty_like(x)
     for li in range(DECODER_LAYERS):
-        att.forward(li, x, x, pos0)
-        rt = ffn.routing_tensors(ffn.route(li, x))
+        att.forward_norm(li, x, x, z, pos0)
+        rt = ffn.routing_tensors(ffn.route(li, z))
         touched.append(int((rt["counts"] > 0).sum()))
-        ffn.forward_layers(li, 1, x)
+        ffn.forward_residual(li, z, x)
     torch.cuda.synchronize()
     out_bits = x.cpu().numpy().view(np.uint16)
     finite = bool(np.isfinite(mi.bf16_bits_to_f32(out_bits)).all())
@@ -471,8 +478,8 @@ def decoder_section(steps, warmup):
     def step():
         x.copy_(x0)
         for li in range(DECODER_LAYERS):
-            att.forward(li, x, x, pos0)
-            ffn.forward_layers(li, 1, x)
+            att.forward_norm(li, x, x, z, pos0)
+            ffn.forward_residual(li, z, x)
 
     for _ in range(warmup):
         step()
@@ -497,9 +504,43 @@ def decoder_section(steps, warmup):
            "hbm_frac": bytes_tok / (ms * 1e-3) / 1e9 / HBM_PEAK_GBS, "output_finite": finite}
     log(f"decoder: {ms:.2f} ms/token ({1e3 / ms:.1f} tok/s), graph {ms_graph:.2f}, "
         f"direct {ms_direct:.2f}, {out['hbm_gbs']:.0f} GB/s")
+    # prompt evaluation: a 2048-token prompt from an empty cache through all
+    # 40 layers (attention on the prefill path, the MoE on the grouped GEMM)
+    P = DECODER_PROMPT
+    xp0 = pool_take(P * aw.d * 2).view(torch.int16).view(P, aw.d)
+    mi.gen_bf16_device(aw.seed, mi.stream_id(mi.KIND_ATTN_X, 1), P * aw.d, aw.sigma_x,
+                       xp0.data_ptr(), s)
+    xp = xp0.clone()
+    zp = pool_take(P * aw.d * 2).view(torch.int16).view(P, aw.d)
+
+    def prompt():
+        xp.copy_(xp0)
+        for li in range(DECODER_LAYERS):
+            att.forward_norm(li, xp, xp, zp, 0)
+            ffn.forward_residual(li, zp, xp)
+
+    prompt()
+    torch.cuda.synchronize()
+    n_pr = 3
+    t0 = time.perf_counter()
+    for _ in range(n_pr):
+        prompt()
+    torch.cuda.synchronize()
+    ms_prompt = (time.perf_counter() - t0) * 1e3 / n_pr
+    pf = np.isfinite(mi.bf16_bits_to_f32(xp.cpu().numpy().view(np.uint16))).all()
+    attn_f = (2.0 * P * aw.d * aw.nqkv + 2.0 * P * aw.n_heads * aw.hd * aw.d +
+              4.0 * aw.n_heads * aw.hd * P * (P + 1) / 2)
+    moe_f = 2.0 * P * sw.k * 3 * sw.d * sw.f
+    pflops = DECODER_LAYERS * (attn_f + moe_f)
+    out["prompt"] = {"T": P, "ms_per_prompt": ms_prompt, "tokens_per_s": P / (ms_prompt * 1e-3),
+                     "tflops": pflops / (ms_prompt * 1e-3) / 1e12,
+                     "mfma_frac": pflops / (ms_prompt * 1e-3) / 1e12 / MFMA_BF16_PEAK_TFLOPS,
+                     "output_finite": bool(pf)}
+    log(f"decoder prompt: {ms_prompt:.1f} ms for {P} tokens ({P / (ms_prompt * 1e-3):.0f} tok/s, "
+        f"{out['prompt']['tflops']:.0f} TFLOP/s)")
     ffn.close()
     att.close()
-    del ffn, att, x, x0
+    del ffn, att, x, x0, z, xp, xp0, zp
     return out
 
 
@@ -653,6 +694,75 @@ def attn_section(steps, warmup, n_rot=N_ROT):
                         "traffic": measured_traffic("attn_qkv", "attn.hip"),
                         "algorithmic_bytes": qkv_b}}
     log(f"attention decode: {best * 1e3:.1f} us/layer ({out['hbm_gbs']:.0f} GB/s), kernels {kern}")
+    layer.close()
+    del layer, stg, stg2, x, y
+    return out
+
+
+def attn_prefill_section(steps, warmup, n_rot=N_ROT, T=2048):
+    """The DBRX self-attention block on a 2048-token prompt from an empty
+    cache (the long-prompt workload's prompt evaluation): norm, the q|k|v
+    and output projections on the grouped GEMM (matrix cores), rotation and
+    cache append, causal attention on the matrix cores, residual.  n_rot
+    seeded layers in turn.  FLOPs per step: the two projections
+    (2 T d (H + 2G) hd + 2 T H hd d) and the causal attention
+    (4 H hd sum_t (t + 1), scores and P V)."""
+    import numpy as np
+    import torch
+    import moe_inputs as mi
+    import paper_2506_23635_amd as moe
+    aw = mi.ATTN_WORKLOADS["attn_decode"].with_(T=T, pos0=0)
+    cfg = moe.make_attn_config(aw.d, aw.n_heads, aw.n_kv, aw.hd, n_layers=n_rot,
+                               max_seq=aw.max_seq, max_tokens=T, rope_theta=aw.theta,
+                               norm_eps=aw.eps)
+    pool_reset()
+    layer = moe.AttnLayer(cfg, arena=pool_take(moe.attn_weight_bytes(cfg)),
+                          cache=pool_take(moe.attn_cache_bytes(cfg)),
+                          workspace=pool_take(moe.attn_workspace_bytes(cfg)))
+    s = layer.stream
+    stg = pool_take(aw.d * aw.nqkv * 2).view(torch.int16)
+    stg2 = pool_take(aw.n_heads * aw.hd * aw.d * 2).view(torch.int16)
+    for li in range(n_rot):
+        mi.gen_bf16_device(aw.seed, mi.stream_id(mi.KIND_WQKV, li), aw.d * aw.nqkv, aw.sigma_qkv,
+                           stg.data_ptr(), s)
+        mi.gen_bf16_device(aw.seed, mi.stream_id(mi.KIND_WO, li), aw.n_heads * aw.hd * aw.d,
+                           aw.sigma_o, stg2.data_ptr(), s)
+        layer.load_layer(li, torch.from_numpy(aw.gamma(li)).cuda(), stg, stg2)
+    x = torch.from_numpy(aw.x().view(np.int16)).cuda()
+    y = torch.empty_like(x)
+    torch.cuda.synchronize()
+    for i in range(max(warmup, n_rot)):
+        layer.forward(i % n_rot, x, y, 0)
+    torch.cuda.synchronize()
+    n = max(steps - steps % n_rot, n_rot)
+    t0 = time.perf_counter()
+    for i in range(n):
+        layer.forward(i % n_rot, x, y, 0)
+    torch.cuda.synchronize()
+    ms = (time.perf_counter() - t0) * 1e3 / n
+    moe.attn_profile_enable(layer.ctx, 8 * n + 8)
+    for i in range(n):
+        layer.forward(i % n_rot, x, y, 0)
+    torch.cuda.synchronize()
+    prof, _ = moe.attn_profile_read(layer.ctx)
+    moe.attn_profile_enable(layer.ctx, 0)
+    kern = {k: v[0] / v[1] for k, v in prof.items() if v[1]}
+    d, nq, nqkv = aw.d, aw.n_heads * aw.hd, aw.nqkv
+    f_qkv = 2.0 * T * d * nqkv
+    f_out = 2.0 * T * nq * d
+    f_att = 4.0 * aw.n_heads * aw.hd * (T * (T + 1) / 2)
+    flops = f_qkv + f_out + f_att
+    out = {"workload": "dbrx_attention_prefill", "T": T, "context": T, "rotation_layers": n_rot,
+           "ms_per_layer": ms, "tokens_per_s": T / (ms * 1e-3), "tflops": flops / (ms * 1e-3) / 1e12,
+           "mfma_frac": flops / (ms * 1e-3) / 1e12 / MFMA_BF16_PEAK_TFLOPS,
+           "kernels_ms": kern,
+           "roofline": {"bound": "mfma", "kernel": "qkv", "achieved": f_qkv / (kern["qkv"] * 1e-3) / 1e12,
+                        "peak": MFMA_BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
+                        "frac": f_qkv / (kern["qkv"] * 1e-3) / 1e12 / MFMA_BF16_PEAK_TFLOPS,
+                        "algorithmic_flops": f_qkv},
+           "attention_core_tflops": f_att / (kern["score"] * 1e-3) / 1e12}
+    log(f"attention prefill: {ms:.3f} ms/layer ({out['tflops']:.0f} TFLOP/s), kernels "
+        f"{ {k: round(v, 3) for k, v in kern.items()} }")
     layer.close()
     del layer, stg, stg2, x, y
     return out
@@ -896,7 +1006,8 @@ def main():
         dst.copy_(src)          # reads 1 GiB, writes 1 GiB
         pool_reset()
     if args.attn_only:
-        print(json.dumps({"attention": attn_section(args.steps, args.warmup)}), flush=True)
+        print(json.dumps({"attention": attn_section(args.steps, args.warmup),
+                          "attention_prefill": attn_prefill_section(8, 2)}), flush=True)
         pool_release()
         return
     if args.prefill_only:
@@ -981,6 +1092,8 @@ def main():
     if not args.no_attn:
         log("timing the attention block (decode) ...")
         attention = attn_section(args.steps, args.warmup)
+        log("timing the attention block (prefill) ...")
+        attention["prefill"] = attn_prefill_section(8, 2)
 
     ep_share = None
     if not args.no_ep_share:

@@ -63,6 +63,7 @@ typedef struct {
 
 /* Bytes of the caller-allocated weight arena (per layer: gamma fp32 [d]
  * padded to 256 B, the rotary frequencies fp64 [head_dim/2] padded to 256 B,
+ * the post-attention norm's gamma2 fp32 [d] padded to 256 B,
  * then Wqkv and Wo repacked into the fragment-tiled layout
  * of moe.h's experts, the query and key rows of Wqkv reordered within each
  * head so that the two members of every rotation pair share a 16-row tile),
@@ -105,6 +106,19 @@ MOE_API moe_status attn_load_layer(attn_ctx *ctx, int32_t layer, const float *ga
 MOE_API moe_status attn_forward(attn_ctx *ctx, int32_t layer, const uint16_t *x, uint16_t *y,
                                 int32_t T, int32_t pos0, moe_stream_t stream);
 
+/* The post-attention norm of a DBRX decoder layer (its attention part is
+ * norm, attention, norm; Sec. 2.1's decoder layer feeds the MoE FFN the
+ * block's output): loads gamma2 fp32 [d] of layer `layer` (src_on_device as
+ * attn_load_layer). */
+MOE_API moe_status attn_load_post_norm(attn_ctx *ctx, int32_t layer, const float *gamma2,
+                                       int32_t src_on_device, moe_stream_t stream);
+
+/* attn_forward, then z = bf16((y - mean) / sqrt(var + eps) * gamma2) (bf16
+ * [T, d]), the normalised input of the layer's MoE FFN; z may be y.
+ * Requires attn_load_post_norm of the layer (MOE_E_STATE). */
+MOE_API moe_status attn_forward_norm(attn_ctx *ctx, int32_t layer, const uint16_t *x, uint16_t *y,
+                                     uint16_t *z, int32_t T, int32_t pos0, moe_stream_t stream);
+
 /* Introspection for tests: device pointers into the workspace with the last
  * forward's intermediates, valid until the next forward: h bf16 [T, d],
  * qkv fp32 [T, (n_heads + 2 n_kv_heads) head_dim] (before rotation), q bf16
@@ -124,7 +138,8 @@ typedef enum {
     ATTN_K_PACK = 5,       /* weight repacking */
     ATTN_K_ROPE = 6,       /* rotary + cache append (prefill) */
     ATTN_K_RESIDUAL = 7,   /* y = bf16(x + o) (prefill) */
-    ATTN_K_COUNT = 8
+    ATTN_K_POST_NORM = 8,  /* z = norm(y) (attn_forward_norm) */
+    ATTN_K_COUNT = 9
 } attn_kernel_kind;
 MOE_API moe_status attn_profile_enable(attn_ctx *ctx, int32_t max_launches);
 MOE_API moe_status attn_profile_read(attn_ctx *ctx, double *total_ms, int64_t *launches,

@@ -230,6 +230,14 @@ MOE_API moe_status moe_forward_stack(moe_ctx *ctx, uint16_t *x_inout, int32_t T,
 MOE_API moe_status moe_forward_layers(moe_ctx *ctx, int32_t first, int32_t n, uint16_t *x_inout,
                                       int32_t T, moe_stream_t stream);
 
+/* Sec. 2.1's decoder layer with the FFN fed a normalised input: layer
+ * `layer` on x (bf16 [T, d], routed and computed as moe_forward), its output
+ * added into the residual stream r_inout = bf16(r_inout + bf16(y)) in place
+ * (bf16 [T, d]; r_inout may be x, which is then one layer of
+ * moe_forward_layers).  Errors as moe_forward_layers. */
+MOE_API moe_status moe_forward_residual(moe_ctx *ctx, int32_t layer, const uint16_t *x,
+                                        uint16_t *r_inout, int32_t T, moe_stream_t stream);
+
 /* Workspace map for a caller that owns the workspace and wants to inspect or
  * guard its parts: region i (moe_ws_region order) starts offset[i] bytes
  * into the workspace and holds bytes[i] bytes; the gaps between regions

@@ -286,6 +286,11 @@ class AttnWorkload:
         g = gen_f32(self.seed, stream_id(KIND_GAMMA, layer), (self.d,), self.sigma_gamma)
         return (np.float32(1.0) + g).astype(np.float32)
 
+    def gamma2(self, layer: int = 0) -> np.ndarray:
+        """The post-attention norm's scale (the MoE FFN's input norm)."""
+        g = gen_f32(self.seed, stream_id(KIND_GAMMA, layer, 1), (self.d,), self.sigma_gamma)
+        return (np.float32(1.0) + g).astype(np.float32)
+
     def wqkv(self, layer: int = 0) -> np.ndarray:
         return gen_bf16(self.seed, stream_id(KIND_WQKV, layer), (self.d, self.nqkv), self.sigma_qkv)
 

@@ -26,16 +26,18 @@ STATUS_NAMES = {0: "MOE_OK", -1: "MOE_E_ARG", -2: "MOE_E_SHAPE", -3: "MOE_E_ALIG
 EXPORTED = ["moe_weight_bytes", "moe_workspace_bytes", "moe_workspace_map", "moe_init",
             "moe_load_expert",
             "moe_load_router", "moe_route", "moe_forward", "moe_forward_static",
-            "moe_forward_stack", "moe_forward_layers",
+            "moe_forward_stack", "moe_forward_layers", "moe_forward_residual",
             "moe_intermediates", "moe_profile_enable", "moe_profile_read",
             "moe_profile_gemm_timeline", "moe_destroy",
             "moe_last_error", "moe_status_string", "moe_diag_stream_read",
             # include/attn.h
             "attn_weight_bytes", "attn_cache_bytes", "attn_workspace_bytes", "attn_init",
-            "attn_load_layer", "attn_forward", "attn_intermediates", "attn_profile_enable",
-            "attn_profile_read", "attn_destroy", "attn_last_error"]
+            "attn_load_layer", "attn_load_post_norm", "attn_forward", "attn_forward_norm",
+            "attn_intermediates", "attn_profile_enable", "attn_profile_read", "attn_destroy",
+            "attn_last_error"]
 
-ATTN_KERNEL_KINDS = ["norm", "qkv", "score", "combine", "out", "pack", "rope", "residual"]
+ATTN_KERNEL_KINDS = ["norm", "qkv", "score", "combine", "out", "pack", "rope", "residual",
+                     "post_norm"]
 
 KERNEL_KINDS = ["router", "route", "decode_gateup", "decode_down", "gemm_gateup", "gemm_down",
                 "combine", "pack"]
@@ -100,6 +102,7 @@ def lib():
         L.moe_forward_static.argtypes = [P, I, P, I, P, P]
         L.moe_forward_stack.argtypes = [P, P, I, P]
         L.moe_forward_layers.argtypes = [P, I, I, P, I, P]
+        L.moe_forward_residual.argtypes = [P, I, P, P, I, P]
         L.moe_intermediates.argtypes = [P, ctypes.POINTER(P), ctypes.POINTER(P)]
         L.moe_profile_enable.argtypes = [P, I]
         L.moe_profile_read.argtypes = [P, P, P, P]
@@ -118,6 +121,8 @@ def lib():
         L.attn_init.argtypes = [acfg, P, P, P, ctypes.POINTER(P)]
         L.attn_load_layer.argtypes = [P, I, P, P, P, I, P]
         L.attn_forward.argtypes = [P, I, P, P, I, I, P]
+        L.attn_load_post_norm.argtypes = [P, I, P, I, P]
+        L.attn_forward_norm.argtypes = [P, I, P, P, P, I, I, P]
         L.attn_intermediates.argtypes = [P] + [ctypes.POINTER(P)] * 5
         L.attn_profile_enable.argtypes = [P, I]
         L.attn_profile_read.argtypes = [P, P, P, P]
@@ -125,11 +130,13 @@ def lib():
         L.attn_destroy.restype = None
         L.attn_last_error.argtypes = [P]
         L.attn_last_error.restype = ctypes.c_char_p
-        for fn in ("attn_init", "attn_load_layer", "attn_forward", "attn_intermediates",
+        for fn in ("attn_init", "attn_load_layer", "attn_load_post_norm", "attn_forward",
+                   "attn_forward_norm", "attn_intermediates",
                    "attn_profile_enable", "attn_profile_read"):
             getattr(L, fn).restype = ctypes.c_int
         for fn in ("moe_init", "moe_load_expert", "moe_load_router", "moe_route", "moe_forward",
                    "moe_forward_static", "moe_forward_stack", "moe_forward_layers",
+                   "moe_forward_residual",
                    "moe_intermediates", "moe_profile_enable",
                    "moe_profile_read", "moe_profile_gemm_timeline", "moe_diag_stream_read"):
             getattr(L, fn).restype = ctypes.c_int
@@ -204,6 +211,10 @@ def moe_forward_stack(ctx, x_ptr, T, stream=0):
 
 def moe_forward_layers(ctx, first, n, x_ptr, T, stream=0):
     _check(ctx, lib().moe_forward_layers(ctx, first, n, x_ptr, T, stream))
+
+
+def moe_forward_residual(ctx, layer, x_ptr, r_ptr, T, stream=0):
+    _check(ctx, lib().moe_forward_residual(ctx, layer, x_ptr, r_ptr, T, stream))
 
 
 def moe_diag_stream_read(src_ptr, nbytes, out_ptr, stream=0):
@@ -381,6 +392,13 @@ class MoeLayer:
         moe_forward_stack(self.ctx, _tensor_ptr(x, "x", T * self.cfg.d_model, _bf16_types(self.torch),
                                                 self.device), T, self.stream)
 
+    def forward_residual(self, layer, x, r, T=None):
+        """moe_forward_residual: r = bf16(r + bf16(layer(x))) in place."""
+        T = self._tokens(x, T)
+        n, bf = T * self.cfg.d_model, _bf16_types(self.torch)
+        moe_forward_residual(self.ctx, layer, _tensor_ptr(x, "x", n, bf, self.device),
+                             _tensor_ptr(r, "r", n, bf, self.device), T, self.stream)
+
     def forward_layers(self, first, n, x, T=None):
         """moe_forward_layers: layers first .. first+n-1, x = bf16(x + y) in place."""
         T = self._tokens(x, T)
@@ -497,6 +515,14 @@ def attn_forward(ctx, layer, x_ptr, y_ptr, T, pos0, stream=0):
     _acheck(ctx, lib().attn_forward(ctx, layer, x_ptr, y_ptr, T, pos0, stream))
 
 
+def attn_load_post_norm(ctx, layer, gamma2_ptr, src_on_device, stream=0):
+    _acheck(ctx, lib().attn_load_post_norm(ctx, layer, gamma2_ptr, src_on_device, stream))
+
+
+def attn_forward_norm(ctx, layer, x_ptr, y_ptr, z_ptr, T, pos0, stream=0):
+    _acheck(ctx, lib().attn_forward_norm(ctx, layer, x_ptr, y_ptr, z_ptr, T, pos0, stream))
+
+
 def attn_intermediates(ctx):
     ptrs = [ctypes.c_void_p() for _ in range(5)]
     _acheck(ctx, lib().attn_intermediates(ctx, *[ctypes.byref(p) for p in ptrs]))
@@ -584,6 +610,21 @@ class AttnLayer:
         n, bf = T * self.cfg.d_model, _bf16_types(self.torch)
         attn_forward(self.ctx, layer, _tensor_ptr(x, "x", n, bf, self.device),
                      _tensor_ptr(y, "y", n, bf, self.device), T, pos0, self.stream)
+
+    def load_post_norm(self, layer, gamma2):
+        on_dev = gamma2.is_cuda
+        dev = self.device if on_dev else self.torch.device("cpu")
+        attn_load_post_norm(self.ctx, layer,
+                            _tensor_ptr(gamma2, "gamma2", self.cfg.d_model, (self.torch.float32,), dev),
+                            int(on_dev), self.stream if on_dev else 0)
+
+    def forward_norm(self, layer, x, y, z, pos0, T=None):
+        """attn_forward_norm: y = x + attention, z = the post-attention norm of y."""
+        T = x.shape[0] if T is None else int(T)
+        n, bf = T * self.cfg.d_model, _bf16_types(self.torch)
+        attn_forward_norm(self.ctx, layer, _tensor_ptr(x, "x", n, bf, self.device),
+                          _tensor_ptr(y, "y", n, bf, self.device),
+                          _tensor_ptr(z, "z", n, bf, self.device), T, pos0, self.stream)
 
     def intermediates(self, T):
         """Copies of the last forward's h, qkv, q, a, o (numpy; bf16 as uint16)."""

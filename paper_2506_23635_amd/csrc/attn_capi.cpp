@@ -30,7 +30,8 @@ constexpr int kMaxGroup = 8;       // query heads per key/value head (attention 
 size_t align_up(size_t v, size_t a) { return (v + a - 1) / a * a; }
 
 struct Layout {
-    size_t gamma_bytes, freq_off, wqkv_off, wqkv_bytes, wo_off, wo_bytes, layer_bytes, arena_bytes;
+    size_t gamma_bytes, freq_off, gamma2_off, wqkv_off, wqkv_bytes, wo_off, wo_bytes, layer_bytes,
+        arena_bytes;
     size_t cache_head_elems, cache_layer_bytes, cache_bytes;
     size_t h_off, qkv_off, q_off, part_off, a_off, o_off, qkvp_off, plan_off, ws_bytes;
     int nqkv, nq, n_chunks, max_tiles;
@@ -68,7 +69,8 @@ Layout make_layout(const attn_config* c)
     L.nqkv = (int)((H + 2 * G) * hd);
     L.gamma_bytes = align_up(d * 4, kAlign);
     L.freq_off = L.gamma_bytes;
-    L.wqkv_off = L.freq_off + align_up(hd / 2 * 8, kAlign);
+    L.gamma2_off = L.freq_off + align_up(hd / 2 * 8, kAlign);
+    L.wqkv_off = L.gamma2_off + L.gamma_bytes;
     L.wqkv_bytes = d * L.nqkv * 2;
     L.wo_off = L.wqkv_off + align_up(L.wqkv_bytes, kAlign);
     L.wo_bytes = (size_t)L.nq * d * 2;
@@ -111,6 +113,7 @@ struct attn_ctx {
     uint8_t* cache;
     uint8_t* ws;
     std::vector<uint8_t> loaded;
+    std::vector<uint8_t> post_loaded;
     bool prof_on;
     std::vector<hipEvent_t> prof_events;
     std::vector<int> prof_kinds;
@@ -230,6 +233,70 @@ moe_status prefill(attn_ctx* ctx, int layer, const uint16_t* x, uint16_t* y, int
 
 }  // namespace
 
+namespace {
+
+moe_status check_forward(attn_ctx* ctx, int32_t layer, const uint16_t* x, uint16_t* y, int32_t T,
+                         int32_t pos0)
+{
+    const attn_config& c = ctx->cfg;
+    if (layer < 0 || layer >= c.n_layers) return fail(ctx, MOE_E_ARG, "layer out of range");
+    if (T < 0 || pos0 < 0) return fail(ctx, MOE_E_ARG, "T and pos0 must be non-negative");
+    if (T > c.max_tokens) return fail(ctx, MOE_E_CAPACITY, "T exceeds max_tokens");
+    if ((int64_t)pos0 + T > c.max_seq) return fail(ctx, MOE_E_CAPACITY, "pos0 + T exceeds max_seq");
+    if (!ctx->loaded[layer]) return fail(ctx, MOE_E_STATE, "layer weights not loaded");
+    if (T == 0) return MOE_OK;
+    if (!x || !y) return fail(ctx, MOE_E_ARG, "x or y is NULL");
+    if (misaligned(x) || misaligned(y)) return fail(ctx, MOE_E_ALIGN, "x and y must be 16-byte aligned");
+    return MOE_OK;
+}
+
+moe_status forward_impl(attn_ctx* ctx, int32_t layer, const uint16_t* x, uint16_t* y, int32_t T,
+                        int32_t pos0, hipStream_t s)
+{
+    const attn_config& c = ctx->cfg;
+    const Layout& L = ctx->L;
+    uint8_t* w = layer_w(ctx, layer);
+    uint16_t* h = reinterpret_cast<uint16_t*>(ctx->ws + L.h_off);
+    float* qkv = reinterpret_cast<float*>(ctx->ws + L.qkv_off);
+    uint16_t* q = reinterpret_cast<uint16_t*>(ctx->ws + L.q_off);
+    float* part = reinterpret_cast<float*>(ctx->ws + L.part_off);
+    uint16_t* a = reinterpret_cast<uint16_t*>(ctx->ws + L.a_off);
+    float* o = reinterpret_cast<float*>(ctx->ws + L.o_off);
+    const int d = c.d_model;
+    const float* gamma = reinterpret_cast<const float*>(w);
+    hipError_t e = hipSuccess;
+    if (T > kDecodeTokens) return prefill(ctx, layer, x, y, T, pos0, s);
+    if (!attn_norm_in_projection(T)) {
+        e = timed(ctx, ATTN_K_NORM, s, [&] {
+            return attn_launch_norm(x, gamma, T, d, c.norm_eps, h, s);
+        });
+        if (e != hipSuccess) return hip_fail(ctx, e, "norm kernel launch");
+    }
+    e = timed(ctx, ATTN_K_QKV, s, [&] {
+        return attn_launch_qkv(w + L.wqkv_off, h, x, gamma, c.norm_eps,
+                               reinterpret_cast<const double*>(w + L.freq_off), qkv, q,
+                               layer_k(ctx, layer), layer_v(ctx, layer), T, d, c.n_heads,
+                               c.n_kv_heads, c.head_dim, c.max_seq, pos0, s);
+    });
+    if (e != hipSuccess) return hip_fail(ctx, e, "projection kernel launch");
+    e = timed(ctx, ATTN_K_SCORE, s, [&] {
+        return attn_launch_score(q, layer_k(ctx, layer), layer_v(ctx, layer), part, T, c.n_heads,
+                                 c.n_kv_heads, c.head_dim, c.max_seq, pos0, L.n_chunks, s);
+    });
+    if (e != hipSuccess) return hip_fail(ctx, e, "attention kernel launch");
+    e = timed(ctx, ATTN_K_COMBINE, s, [&] {
+        return attn_launch_combine(part, a, T, c.n_heads, c.head_dim, pos0, L.n_chunks, s);
+    });
+    if (e != hipSuccess) return hip_fail(ctx, e, "merge kernel launch");
+    e = timed(ctx, ATTN_K_OUT, s, [&] {
+        return attn_launch_out(w + L.wo_off, a, T, L.nq, d, o, x, y, s);
+    });
+    if (e != hipSuccess) return hip_fail(ctx, e, "output projection kernel launch");
+    return MOE_OK;
+}
+
+}  // namespace
+
 extern "C" {
 
 size_t attn_weight_bytes(const attn_config* cfg)
@@ -282,6 +349,7 @@ moe_status attn_init(const attn_config* cfg, void* weight_arena, void* kv_cache,
         }
     }
     c->loaded.assign(cfg->n_layers, 0);
+    c->post_loaded.assign(cfg->n_layers, 0);
     c->prof_on = false;
     c->prof_dropped = 0;
     *out = c;
@@ -342,58 +410,55 @@ moe_status attn_load_layer(attn_ctx* ctx, int32_t layer, const float* gamma, con
     return MOE_OK;
 }
 
+moe_status attn_load_post_norm(attn_ctx* ctx, int32_t layer, const float* gamma2,
+                               int32_t src_on_device, moe_stream_t stream)
+{
+    if (!ctx) return MOE_E_ARG;
+    if (layer < 0 || layer >= ctx->cfg.n_layers) return fail(ctx, MOE_E_ARG, "layer out of range");
+    if (!gamma2) return fail(ctx, MOE_E_ARG, "gamma2 is NULL");
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    uint8_t* dst = layer_w(ctx, layer) + ctx->L.gamma2_off;
+    const size_t bytes = (size_t)ctx->cfg.d_model * 4;
+    hipError_t e;
+    if (src_on_device) {
+        if (misaligned(gamma2)) return fail(ctx, MOE_E_ALIGN, "gamma2 must be 16-byte aligned");
+        e = hipMemcpyAsync(dst, gamma2, bytes, hipMemcpyDeviceToDevice, s);
+    } else {
+        e = hipMemcpyAsync(dst, gamma2, bytes, hipMemcpyHostToDevice, s);
+        if (e == hipSuccess) e = hipStreamSynchronize(s);
+    }
+    if (e != hipSuccess) return hip_fail(ctx, e, "post-attention norm load");
+    ctx->post_loaded[layer] = 1;
+    return MOE_OK;
+}
+
 moe_status attn_forward(attn_ctx* ctx, int32_t layer, const uint16_t* x, uint16_t* y, int32_t T,
                         int32_t pos0, moe_stream_t stream)
 {
     if (!ctx) return MOE_E_ARG;
-    const attn_config& c = ctx->cfg;
-    const Layout& L = ctx->L;
-    if (layer < 0 || layer >= c.n_layers) return fail(ctx, MOE_E_ARG, "layer out of range");
-    if (T < 0 || pos0 < 0) return fail(ctx, MOE_E_ARG, "T and pos0 must be non-negative");
-    if (T > c.max_tokens) return fail(ctx, MOE_E_CAPACITY, "T exceeds max_tokens");
-    if ((int64_t)pos0 + T > c.max_seq) return fail(ctx, MOE_E_CAPACITY, "pos0 + T exceeds max_seq");
-    if (!ctx->loaded[layer]) return fail(ctx, MOE_E_STATE, "layer weights not loaded");
+    moe_status st = check_forward(ctx, layer, x, y, T, pos0);
+    if (st != MOE_OK || T == 0) return st;
+    return forward_impl(ctx, layer, x, y, T, pos0, static_cast<hipStream_t>(stream));
+}
+
+moe_status attn_forward_norm(attn_ctx* ctx, int32_t layer, const uint16_t* x, uint16_t* y,
+                             uint16_t* z, int32_t T, int32_t pos0, moe_stream_t stream)
+{
+    if (!ctx) return MOE_E_ARG;
+    moe_status st = check_forward(ctx, layer, x, y, T, pos0);
+    if (st != MOE_OK) return st;
+    if (!ctx->post_loaded[layer]) return fail(ctx, MOE_E_STATE, "post-attention norm not loaded");
     if (T == 0) return MOE_OK;
-    if (!x || !y) return fail(ctx, MOE_E_ARG, "x or y is NULL");
-    if (misaligned(x) || misaligned(y)) return fail(ctx, MOE_E_ALIGN, "x and y must be 16-byte aligned");
+    if (!z) return fail(ctx, MOE_E_ARG, "z is NULL");
+    if (misaligned(z)) return fail(ctx, MOE_E_ALIGN, "z must be 16-byte aligned");
     hipStream_t s = static_cast<hipStream_t>(stream);
-    uint8_t* w = layer_w(ctx, layer);
-    uint16_t* h = reinterpret_cast<uint16_t*>(ctx->ws + L.h_off);
-    float* qkv = reinterpret_cast<float*>(ctx->ws + L.qkv_off);
-    uint16_t* q = reinterpret_cast<uint16_t*>(ctx->ws + L.q_off);
-    float* part = reinterpret_cast<float*>(ctx->ws + L.part_off);
-    uint16_t* a = reinterpret_cast<uint16_t*>(ctx->ws + L.a_off);
-    float* o = reinterpret_cast<float*>(ctx->ws + L.o_off);
-    const int d = c.d_model;
-    const float* gamma = reinterpret_cast<const float*>(w);
-    hipError_t e = hipSuccess;
-    if (T > kDecodeTokens) return prefill(ctx, layer, x, y, T, pos0, s);
-    if (!attn_norm_in_projection(T)) {
-        e = timed(ctx, ATTN_K_NORM, s, [&] {
-            return attn_launch_norm(x, gamma, T, d, c.norm_eps, h, s);
-        });
-        if (e != hipSuccess) return hip_fail(ctx, e, "norm kernel launch");
-    }
-    e = timed(ctx, ATTN_K_QKV, s, [&] {
-        return attn_launch_qkv(w + L.wqkv_off, h, x, gamma, c.norm_eps,
-                               reinterpret_cast<const double*>(w + L.freq_off), qkv, q,
-                               layer_k(ctx, layer), layer_v(ctx, layer), T, d, c.n_heads,
-                               c.n_kv_heads, c.head_dim, c.max_seq, pos0, s);
+    st = forward_impl(ctx, layer, x, y, T, pos0, s);
+    if (st != MOE_OK) return st;
+    const float* gamma2 = reinterpret_cast<const float*>(layer_w(ctx, layer) + ctx->L.gamma2_off);
+    const hipError_t e = timed(ctx, ATTN_K_POST_NORM, s, [&] {
+        return attn_launch_norm(y, gamma2, T, ctx->cfg.d_model, ctx->cfg.norm_eps, z, s);
     });
-    if (e != hipSuccess) return hip_fail(ctx, e, "projection kernel launch");
-    e = timed(ctx, ATTN_K_SCORE, s, [&] {
-        return attn_launch_score(q, layer_k(ctx, layer), layer_v(ctx, layer), part, T, c.n_heads,
-                                 c.n_kv_heads, c.head_dim, c.max_seq, pos0, L.n_chunks, s);
-    });
-    if (e != hipSuccess) return hip_fail(ctx, e, "attention kernel launch");
-    e = timed(ctx, ATTN_K_COMBINE, s, [&] {
-        return attn_launch_combine(part, a, T, c.n_heads, c.head_dim, pos0, L.n_chunks, s);
-    });
-    if (e != hipSuccess) return hip_fail(ctx, e, "merge kernel launch");
-    e = timed(ctx, ATTN_K_OUT, s, [&] {
-        return attn_launch_out(w + L.wo_off, a, T, L.nq, d, o, x, y, s);
-    });
-    if (e != hipSuccess) return hip_fail(ctx, e, "output projection kernel launch");
+    if (e != hipSuccess) return hip_fail(ctx, e, "post-attention norm launch");
     return MOE_OK;
 }
 

@@ -583,6 +583,27 @@ moe_status moe_forward_layers(moe_ctx* ctx, int32_t first, int32_t n, uint16_t* 
     return MOE_OK;
 }
 
+moe_status moe_forward_residual(moe_ctx* ctx, int32_t layer, const uint16_t* x, uint16_t* r_inout,
+                                int32_t T, moe_stream_t stream)
+{
+    if (!ctx) return MOE_E_ARG;
+    if (layer < 0 || layer >= ctx->cfg.n_layers) return fail(ctx, MOE_E_ARG, "layer out of range");
+    if (T < 0) return fail(ctx, MOE_E_ARG, "T is negative");
+    if (T > ctx->cfg.max_tokens) return fail(ctx, MOE_E_CAPACITY, "T exceeds max_tokens");
+    moe_status st = check_layer(ctx, layer);
+    if (st != MOE_OK) return st;
+    if (T == 0) return MOE_OK;
+    if (!x || !r_inout) return fail(ctx, MOE_E_ARG, "x or r is NULL");
+    if (misaligned(x) || misaligned(r_inout)) return fail(ctx, MOE_E_ALIGN, "x and r must be 16-byte aligned");
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    ctx->route_valid = false;   // the routing views are about to be overwritten
+    st = do_route(ctx, ctx->ws, layer, x, T, nullptr, s);
+    if (st != MOE_OK) return st;
+    st = run_experts(ctx, ctx->ws, layer, x, T, s);
+    if (st != MOE_OK) return st;
+    return combine(ctx, ctx->ws, T, nullptr, nullptr, r_inout, s);
+}
+
 moe_status moe_forward_stack(moe_ctx* ctx, uint16_t* x_inout, int32_t T, moe_stream_t stream)
 {
     if (!ctx) return MOE_E_ARG;

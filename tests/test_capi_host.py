@@ -153,6 +153,9 @@ def test_ctx_validation_before_any_launch(fake_ctx):
     assert L.moe_forward_layers(fake_ctx, 0, -1, 4096, 1, None) == E_ARG
     assert L.moe_forward_layers(fake_ctx, 0, 0, 4096, 1, None) == 0          # empty range
     assert L.moe_forward_layers(fake_ctx, 0, 1, 4096, 99, None) == E_CAPACITY
+    assert L.moe_forward_residual(fake_ctx, 0, 4096, 8192, 1, None) == E_STATE
+    assert L.moe_forward_residual(fake_ctx, 2, 4096, 8192, 1, None) == E_ARG
+    assert L.moe_forward_residual(fake_ctx, 0, 4096, 8192, 99, None) == E_CAPACITY
     # experts outside the local range [2, 6), null and misaligned pointers
     assert L.moe_load_expert(fake_ctx, 0, 1, 4096, 4096, 4096, 1, None) == E_ARG
     assert L.moe_load_expert(fake_ctx, 0, 6, 4096, 4096, 4096, 1, None) == E_ARG
@@ -250,7 +253,7 @@ def _attn_cfg(**kw):
 
 def test_attn_sizes():
     cfg = _attn_cfg()
-    layer = 6144 * 4 + 512 + (6144 * 8192 + 6144 * 6144) * 2     # gamma, frequencies, Wqkv, Wo
+    layer = 6144 * 4 + 512 + 6144 * 4 + (6144 * 8192 + 6144 * 6144) * 2   # gamma, frequencies, gamma2, Wqkv, Wo
     assert moe.attn_weight_bytes(cfg) == layer
     assert moe.attn_cache_bytes(_attn_cfg(n_layers=3)) == 3 * 2 * 8 * 4096 * 128 * 2
     assert moe.attn_workspace_bytes(cfg) > 16 * (6144 * 2 + 8192 * 4)
@@ -293,5 +296,9 @@ def test_attn_validation_before_any_launch():
         assert L.attn_load_layer(ctx, 0, 4096 + 4, 4096, 4096, 1, None) == E_ALIGN
         assert L.attn_load_layer(ctx, 5, 4096, 4096, 4096, 1, None) == E_ARG
         assert "range" in moe.lib().attn_last_error(ctx).decode()
+        assert L.attn_forward_norm(ctx, 0, 4096, 4096, 4096, 1, 0, None) == E_STATE
+        assert L.attn_load_post_norm(ctx, 0, None, 1, None) == E_ARG
+        assert L.attn_load_post_norm(ctx, 0, 4096 + 4, 1, None) == E_ALIGN
+        assert L.attn_load_post_norm(ctx, 2, 4096, 1, None) == E_ARG
     finally:
         L.attn_destroy(ctx)

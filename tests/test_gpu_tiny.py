@@ -611,6 +611,32 @@ def test_forward_layers_is_the_stack_in_pieces(torch_mod):
     layer.close()
 
 
+def test_forward_residual(torch_mod):
+    """moe_forward_residual adds layer(x) into another stream r bit for bit
+    as moe_forward plus the bf16 residual, and with r = x it is one layer of
+    moe_forward_layers."""
+    torch = torch_mod
+    wl = TINY.with_(T=4, n_layers=2)
+    layer = make_layer(wl, max_tokens=300)
+    for li in range(2):
+        load_workload_host(layer, wl, layer_idx=li)
+    for T in (4, 300):                          # decode GEMVs, then the grouped GEMM
+        x_t, x = x_device(wl, T=T)
+        r_t, r = x_device(wl, layer_idx=1, T=T)
+        y = torch.empty_like(x_t)
+        layer.forward(1, x_t, y)
+        got = r_t.clone()
+        layer.forward_residual(1, x_t, got)
+        same = x_t.clone()
+        layer.forward_residual(1, same, same)
+        ref = x_t.clone()
+        layer.forward_layers(1, 1, ref)
+        torch.cuda.synchronize()
+        assert np.array_equal(to_np_u16(got), oracle.residual_add(r, to_np_u16(y)))
+        assert np.array_equal(to_np_u16(same), to_np_u16(ref))
+    layer.close()
+
+
 @pytest.mark.parametrize("nbytes", [16, (1 << 20) + 48, (200 << 20) + 16])
 def test_diag_stream_read_reads_every_word_once(torch_mod, nbytes):
     """The bench's streaming-read ceiling: the XOR of the per-workgroup XORs
