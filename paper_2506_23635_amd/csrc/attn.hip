@@ -733,7 +733,9 @@ __global__ __launch_bounds__(256) void flash_kernel(FlashArgs a)
     constexpr int VROW = kFlashP + 8;        // padded V^T row (positions, bf16)
     __shared__ __attribute__((aligned(16))) uint16_t ks[kFlashP * KROW];
     __shared__ __attribute__((aligned(16))) uint16_t vt[HD * VROW];
-    const int j = blockIdx.x, qb = blockIdx.y;
+    // the longest query blocks (the most positions) are dispatched first, so
+    // that the last workgroups to start are the short ones
+    const int j = blockIdx.x, qb = gridDim.y - 1 - blockIdx.y;
     const int kvh = j / (a.H / a.G);
     const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
     const int c = lane & 15, grp = lane >> 4;
