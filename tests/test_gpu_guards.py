@@ -6,7 +6,8 @@ expert-parallel share and the stack, every margin must be intact (no kernel
 writes outside the buffers it was given).  Inside the workspace, every
 sub-buffer (moe_workspace_map) is guarded too: after a forward, the bytes of
 each region past what the call may write there, and the padding between
-regions, still hold the pattern."""
+regions, still hold the pattern.  The attention block's arena, cache,
+workspace, input and outputs are guarded the same way."""
 import numpy as np
 import pytest
 
@@ -166,5 +167,48 @@ def test_workspace_regions_stay_inside_themselves(torch_mod, T, e_begin, n_local
         where = [n for n, (o, nb) in m.items() if bad.size and o <= bad[0] < o + nb]
         assert bad.size == 0, (int(bad[0]), where)
         assert ws.intact() and arena.intact()
+    finally:
+        layer.close()
+
+
+ATTN = mi.ATTN_WORKLOADS["attn_tiny"]
+
+
+@pytest.mark.parametrize("T,pos0", [(1, 29), (4, 29), (16, 100), (40, 0), (130, 37)])
+def test_attention_stays_inside_its_buffers(torch_mod, T, pos0):
+    """The attention block (decode and prefill paths, with the post-attention
+    norm) on layer 1 of 2: the margins of its arena, cache, workspace, input
+    and outputs hold, layer 0's cache is untouched, and in layer 1's cache
+    only the new positions change."""
+    import paper_2506_23635_amd as moe
+    torch = torch_mod
+    aw = ATTN.with_(T=T, pos0=pos0)
+    max_seq = 256
+    cfg = moe.make_attn_config(aw.d, aw.n_heads, aw.n_kv, aw.hd, n_layers=2, max_seq=max_seq,
+                               max_tokens=256, rope_theta=aw.theta, norm_eps=aw.eps)
+    arena = Guarded(torch, moe.attn_weight_bytes(cfg))
+    cache = Guarded(torch, moe.attn_cache_bytes(cfg))
+    ws = Guarded(torch, moe.attn_workspace_bytes(cfg))
+    cache.inner.fill_(0x5A)
+    layer = moe.AttnLayer(cfg, arena=arena.inner, cache=cache.inner, workspace=ws.inner)
+    try:
+        for li in range(2):
+            layer.load_layer(li, torch.from_numpy(aw.gamma(li)), torch.from_numpy(aw.wqkv(li).view(np.int16)),
+                             torch.from_numpy(aw.wo(li).view(np.int16)))
+            layer.load_post_norm(li, torch.from_numpy(aw.gamma2(li)))
+        n = T * aw.d * 2
+        x, y, z = Guarded(torch, n), Guarded(torch, n), Guarded(torch, n)
+        x.inner.copy_(torch.from_numpy(aw.x().view(np.uint8).reshape(-1)).cuda())
+        as_bf = lambda g: g.inner.view(torch.int16).view(T, aw.d)
+        layer.forward_norm(1, as_bf(x), as_bf(y), as_bf(z), pos0)
+        torch.cuda.synchronize()
+        for g in (arena, cache, ws, x, y, z):
+            assert g.intact()
+        c = cache.inner.cpu().numpy()
+        per_layer = c.size // 2
+        assert np.all(c[:per_layer] == 0x5A)
+        kv = c[per_layer:].reshape(2, aw.n_kv, max_seq, aw.hd * 2)
+        assert np.all(kv[:, :, :pos0] == 0x5A) and np.all(kv[:, :, pos0 + T:] == 0x5A)
+        assert not np.all(kv[:, :, pos0:pos0 + T] == 0x5A)
     finally:
         layer.close()
