@@ -4,7 +4,9 @@ buffer is refilled between replays with two different token sets, so the
 replays also show that routing, permutation and tile lists are recomputed on
 the device from the current input (nothing host-side is frozen at capture).
 Eager work and synchronisations run between the replays.  Covers the decode
-GEMVs (T = 4), the grouped GEMM (T = 300) and the chained stack."""
+GEMVs (T = 4), the grouped GEMM (T = 300), the chained stack, and two
+decoder layers (attention block with its norms, then the MoE layer) at
+decode and through the prefill path."""
 import numpy as np
 import pytest
 
@@ -106,3 +108,69 @@ def test_stack_graph_replays_match_eager(torch_mod):
         del g
     finally:
         layer.close()
+
+
+ATTN = mi.ATTN_WORKLOADS["attn_tiny"]
+
+
+@pytest.mark.parametrize("T,pos0", [(1, 29), (40, 0)])
+def test_decoder_layers_graph_replays_match_eager(torch_mod, T, pos0):
+    """Two DBRX decoder layers (attn_forward_norm, then moe_forward_residual
+    on the normalised input) captured once and replayed, at decode (T = 1:
+    the norm inside the projection, attention over position chunks) and
+    through the prefill path (T = 40: projection GEMMs, causal attention):
+    every replay equals the eager chain, for two alternating inputs.  The
+    key/value cache positions a call appends are rewritten by every replay."""
+    import paper_2506_23635_amd as moe
+    torch = torch_mod
+    aw = ATTN.with_(T=T, pos0=pos0)
+    wl = TINY.with_(T=T, n_layers=2)
+    acfg = moe.make_attn_config(aw.d, aw.n_heads, aw.n_kv, aw.hd, n_layers=2, max_seq=128,
+                                max_tokens=64, rope_theta=aw.theta, norm_eps=aw.eps)
+    att = moe.AttnLayer(acfg)
+    ffn = make_layer(wl, max_tokens=64, n_layers=2)
+    try:
+        for li in range(2):
+            att.load_layer(li, torch.from_numpy(aw.gamma(li)), torch.from_numpy(aw.wqkv(li).view(np.int16)),
+                           torch.from_numpy(aw.wo(li).view(np.int16)))
+            att.load_post_norm(li, torch.from_numpy(aw.gamma2(li)))
+            K, V = att.cache_views(li)
+            K.zero_()
+            V.zero_()
+            if pos0:
+                k0, v0 = aw.cache_prefix(li)
+                K[:, :pos0] = torch.from_numpy(np.ascontiguousarray(k0.transpose(1, 0, 2)).view(np.int16)).cuda()
+                V[:, :pos0] = torch.from_numpy(np.ascontiguousarray(v0.transpose(1, 0, 2)).view(np.int16)).cuda()
+            load_workload_host(ffn, wl, layer_idx=li)
+        xs = _inputs(torch, wl, T)
+        x0 = xs[0].clone()
+        x = x0.clone()
+        z = torch.empty_like(x)
+
+        def step():
+            x.copy_(x0)
+            for li in range(2):
+                att.forward_norm(li, x, x, z, pos0)
+                ffn.forward_residual(li, z, x)
+
+        refs = []
+        for v in xs:
+            x0.copy_(v)
+            step()
+            torch.cuda.synchronize()
+            refs.append(x.clone())
+        assert not torch.equal(refs[0], refs[1])
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g):
+            step()
+        for i in range(REPLAYS):
+            x0.copy_(xs[i % 2])
+            x.fill_(0x3F80)
+            g.replay()
+            torch.cuda.synchronize()
+            assert torch.equal(x, refs[i % 2]), f"replay {i}"
+            _noise(torch)
+        del g
+    finally:
+        att.close()
+        ffn.close()
