@@ -713,8 +713,11 @@ struct FlashArgs {
     const uint16_t* vc;
     uint16_t* out;         // a [T][H * HD] bf16
     int T, H, G, max_seq, pos0;
-    float scale;
+    int nqb;               // query blocks of kFlashQ tokens
+    float scale2;          // 1/sqrt(head_dim) * log2(e): scores in base 2
 };
+
+constexpr int kXcds = 8;
 
 constexpr int kFlashQ = 64;     // query tokens per workgroup
 constexpr int kFlashP = 64;     // positions per step
@@ -724,8 +727,21 @@ __device__ inline uint32_t pack_bf16x2(float lo, float hi)
     return (uint32_t)moe::f32_to_bf16(lo) | ((uint32_t)moe::f32_to_bf16(hi) << 16);
 }
 
+// Two fp32 -> packed bf16 by one hardware conversion (round to nearest even;
+// used on finite values only, where it equals f32_to_bf16)
+__device__ inline uint32_t cvt_pk_bf16(float lo, float hi)
+{
+    typedef float f32x2_v __attribute__((ext_vector_type(2)));
+    typedef __bf16 bf16x2_v __attribute__((ext_vector_type(2)));
+    const f32x2_v in = {lo, hi};
+    return __builtin_bit_cast(uint32_t, __builtin_convertvector(in, bf16x2_v));
+}
+
+// Three workgroups per CU (the register cap keeps 3 waves per SIMD; with
+// the staging loads all in flight the compiler would otherwise take 172
+// registers and leave room for 2).
 template <int HD>
-__global__ __launch_bounds__(256) void flash_kernel(FlashArgs a)
+__global__ __launch_bounds__(256, 3) void flash_kernel(FlashArgs a)
 {
     constexpr int KS = HD / 32;              // K steps of the score MFMAs
     constexpr int DB = HD / 16;              // 16-dim blocks of the output
@@ -733,13 +749,23 @@ __global__ __launch_bounds__(256) void flash_kernel(FlashArgs a)
     constexpr int VROW = kFlashP + 8;        // padded V^T row (positions, bf16)
     __shared__ __attribute__((aligned(16))) uint16_t ks[kFlashP * KROW];
     __shared__ __attribute__((aligned(16))) uint16_t vt[HD * VROW];
-    // the longest query blocks (the most positions) are dispatched first, so
-    // that the last workgroups to start are the short ones
-    const int j = blockIdx.x, qb = gridDim.y - 1 - blockIdx.y;
-    const int kvh = j / (a.H / a.G);
+    // XCD-aware numbering: hardware hands block b to XCD b % 8, and each XCD
+    // takes a contiguous run of the logical order (key/value head, query
+    // block from the last, query head of the group), so the workgroups of
+    // one key/value head share its K and V in one L2 (DBRX: one head per
+    // XCD) and on every XCD the longest query blocks (the most positions)
+    // start first.  Logical slots past the last block exit at once.
+    const int groups = a.H / a.G;
+    const int per_xcd = gridDim.x / kXcds;
+    const int logical = (blockIdx.x % kXcds) * per_xcd + blockIdx.x / kXcds;
+    if (logical >= a.H * a.nqb) return;
+    const int kvh = logical / (a.nqb * groups), rem = logical % (a.nqb * groups);
+    const int qb = a.nqb - 1 - rem / groups;
+    const int j = kvh * groups + rem % groups;
     const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
     const int c = lane & 15, grp = lane >> 4;
-    const int t = qb * kFlashQ + w * 16 + c;            // this lane's token
+    const int t_w0 = qb * kFlashQ + w * 16;             // the wave's first token
+    const int t = t_w0 + c;                              // this lane's token
     const bool tok_ok = t < a.T;
     const int lim = a.pos0 + t;                          // its last position
     const u32x4_t zero = {0u, 0u, 0u, 0u};
@@ -761,27 +787,52 @@ __global__ __launch_bounds__(256) void flash_kernel(FlashArgs a)
     const uint16_t* kbase = a.kc + (int64_t)kvh * a.max_seq * HD;
     const uint16_t* vbase = a.vc + (int64_t)kvh * a.max_seq * HD;
     uint32_t* vt32 = reinterpret_cast<uint32_t*>(vt);
+    // per step a thread stages KL 16-byte pieces of K rows and VL position
+    // pairs of V; all of a step's global loads are issued before the barrier
+    // that frees the LDS, so the step waits for one load latency, not one per
+    // piece
+    constexpr int KL = kFlashP * (HD / 8) / 256;
+    constexpr int VL = (kFlashP / 2) * (HD / 8) / 256;
+    static_assert(KL * 256 == kFlashP * (HD / 8) && VL * 256 == (kFlashP / 2) * (HD / 8),
+                  "the staging pieces divide evenly over the 256 threads");
     for (int p0 = 0; p0 < n_pos; p0 += kFlashP) {
         const int live = min(kFlashP, n_pos - p0);
-        __syncthreads();                                 // the last step's LDS reads are done
-        // K rows: 16-byte pieces, coalesced
-        for (int e = threadIdx.x; e < kFlashP * (HD / 8); e += 256) {
+        u32x4_t kv[KL], va[VL], vb[VL];
+#pragma unroll
+        for (int i = 0; i < KL; ++i) {
+            const int e = threadIdx.x + i * 256;
             const int p = e / (HD / 8), k8 = e % (HD / 8);
-            const u32x4_t v = ld16(kbase + (int64_t)(p0 + min(p, live - 1)) * HD + k8 * 8);
-            *reinterpret_cast<u32x4_t*>(&ks[p * KROW + k8 * 8]) = p < live ? v : zero;
+            kv[i] = ld16(kbase + (int64_t)(p0 + min(p, live - 1)) * HD + k8 * 8);
+        }
+#pragma unroll
+        for (int i = 0; i < VL; ++i) {
+            const int e = threadIdx.x + i * 256;
+            const int pp = e % (kFlashP / 2), k8 = e / (kFlashP / 2);
+            va[i] = ld16(vbase + (int64_t)(p0 + min(2 * pp, live - 1)) * HD + k8 * 8);
+            vb[i] = ld16(vbase + (int64_t)(p0 + min(2 * pp + 1, live - 1)) * HD + k8 * 8);
+        }
+        __syncthreads();                                 // the last step's LDS reads are done
+        // K rows: 16-byte pieces, coalesced.  Rows past `live` repeat the
+        // last live row (the loads are clamped): every token's causal mask
+        // removes those positions, so their scores never count and their
+        // probabilities are exactly 0 against finite V rows.
+#pragma unroll
+        for (int i = 0; i < KL; ++i) {
+            const int e = threadIdx.x + i * 256;
+            const int p = e / (HD / 8), k8 = e % (HD / 8);
+            *reinterpret_cast<u32x4_t*>(&ks[p * KROW + k8 * 8]) = kv[i];
         }
         // V transposed: a thread takes positions 2 pp, 2 pp + 1 at 8 dims and
-        // writes 8 words of (position pair) per dim
-        for (int e = threadIdx.x; e < (kFlashP / 2) * (HD / 8); e += 256) {
-            const int pp = e % (kFlashP / 2), k8 = e / (kFlashP / 2);
-            const int pa = 2 * pp, pb = 2 * pp + 1;
-            const u32x4_t va = ld16(vbase + (int64_t)(p0 + min(pa, live - 1)) * HD + k8 * 8);
-            const u32x4_t vb = ld16(vbase + (int64_t)(p0 + min(pb, live - 1)) * HD + k8 * 8);
+        // writes 8 words of (position pair) per dim, each one byte permute
+        // (low halves of the two words, then the high halves)
 #pragma unroll
-            for (int i = 0; i < 4; ++i) {
-                const uint32_t a0 = pa < live ? va[i] : 0u, b0 = pb < live ? vb[i] : 0u;
-                vt32[((k8 * 8 + 2 * i) * VROW) / 2 + pp] = (a0 & 0xFFFFu) | (b0 << 16);
-                vt32[((k8 * 8 + 2 * i + 1) * VROW) / 2 + pp] = (a0 >> 16) | (b0 & 0xFFFF0000u);
+        for (int i = 0; i < VL; ++i) {
+            const int e = threadIdx.x + i * 256;
+            const int pp = e % (kFlashP / 2), k8 = e / (kFlashP / 2);
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+                vt32[((k8 * 8 + 2 * r) * VROW) / 2 + pp] = __builtin_amdgcn_perm(vb[i][r], va[i][r], 0x05040100u);
+                vt32[((k8 * 8 + 2 * r + 1) * VROW) / 2 + pp] = __builtin_amdgcn_perm(vb[i][r], va[i][r], 0x07060302u);
             }
         }
         __syncthreads();
@@ -797,48 +848,67 @@ __global__ __launch_bounds__(256) void flash_kernel(FlashArgs a)
                 st[pb] = moe::mfma16x16x32(kf, qf[k], st[pb]);
             }
         }
-        // scale, causal mask, running maximum and sum of token c
+        // scores in base 2 (s * scale * log2 e, so p = 2^(s2 - m2)); the
+        // causal mask and the tokens past T only on the steps that need them
+        // (wave-uniform: a step past the wave's first token's last position,
+        // or a wave with tokens past T)
         float sv[16];
         float mx = -INFINITY;
+        if (p0 + kFlashP - 1 > a.pos0 + t_w0 || t_w0 + 15 >= a.T) {
 #pragma unroll
-        for (int pb = 0; pb < 4; ++pb)
+            for (int pb = 0; pb < 4; ++pb)
 #pragma unroll
-            for (int r = 0; r < 4; ++r) {
-                const int pos = p0 + pb * 16 + 4 * grp + r;
-                const float v = (tok_ok && pos <= lim) ? st[pb][r] * a.scale : -INFINITY;
-                sv[pb * 4 + r] = v;
-                mx = fmaxf(mx, v);
-            }
+                for (int r = 0; r < 4; ++r) {
+                    const int pos = p0 + pb * 16 + 4 * grp + r;
+                    const float v = (tok_ok && pos <= lim) ? st[pb][r] * a.scale2 : -INFINITY;
+                    sv[pb * 4 + r] = v;
+                    mx = fmaxf(mx, v);
+                }
+        } else {
+#pragma unroll
+            for (int pb = 0; pb < 4; ++pb)
+#pragma unroll
+                for (int r = 0; r < 4; ++r) {
+                    sv[pb * 4 + r] = st[pb][r] * a.scale2;
+                    mx = fmaxf(mx, sv[pb * 4 + r]);
+                }
+        }
         mx = fmaxf(mx, __shfl_xor(mx, 16, 64));
         mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
         const float mn = fmaxf(m, mx);
-        const float alpha = m == -INFINITY ? 0.f : expf(m - mn);
+        // a token with every position masked so far (only tokens past T)
+        // keeps mn = -inf: subtract 0 instead, so its p are 0, not NaN
+        const float msub = mn == -INFINITY ? 0.f : mn;
         float ps = 0.f;
         float pv[16];
 #pragma unroll
         for (int e = 0; e < 16; ++e) {
-            pv[e] = sv[e] == -INFINITY ? 0.f : expf(sv[e] - mn);
+            pv[e] = __builtin_amdgcn_exp2f(sv[e] - msub);
             ps += pv[e];
         }
         ps += __shfl_xor(ps, 16, 64);
         ps += __shfl_xor(ps, 32, 64);
-        l = l * alpha + ps;
-        m = mn;
+        // rescale the running sums only where a maximum moved (m == mn gives
+        // the factor 1 exactly, so skipping it changes no bit)
+        if (__ballot(mn != m)) {
+            const float alpha = m == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(m - mn);
+            l *= alpha;
 #pragma unroll
-        for (int b = 0; b < DB; ++b) o[b] *= alpha;
-        // O^T += V^T P^T over the two 32-position K blocks, P as hi + lo
+            for (int b = 0; b < DB; ++b) o[b] *= alpha;
+        }
+        l += ps;
+        m = mn;
+        // O^T += V^T P^T over the two 32-position K blocks, P as hi + lo:
+        // hi = bf16(p), lo = bf16(p - hi) (the subtraction is exact)
 #pragma unroll
         for (int kb = 0; kb < 2; ++kb) {
             u32x4_t bh, bl;
 #pragma unroll
-            for (int i = 0; i < 2; ++i) {
-                const float* pq = &pv[(2 * kb + i) * 4];
-                const float h0 = bf16_round(pq[0]), h1 = bf16_round(pq[1]);
-                const float h2 = bf16_round(pq[2]), h3 = bf16_round(pq[3]);
-                bh[2 * i] = pack_bf16x2(h0, h1);
-                bh[2 * i + 1] = pack_bf16x2(h2, h3);
-                bl[2 * i] = pack_bf16x2(pq[0] - h0, pq[1] - h1);
-                bl[2 * i + 1] = pack_bf16x2(pq[2] - h2, pq[3] - h3);
+            for (int i = 0; i < 4; ++i) {
+                const float p0v = pv[kb * 8 + 2 * i], p1v = pv[kb * 8 + 2 * i + 1];
+                const uint32_t h = cvt_pk_bf16(p0v, p1v);
+                bh[i] = h;
+                bl[i] = cvt_pk_bf16(p0v - __uint_as_float(h << 16), p1v - __uint_as_float(h & 0xFFFF0000u));
             }
 #pragma unroll
             for (int b = 0; b < DB; ++b) {
@@ -950,8 +1020,10 @@ hipError_t attn_launch_flash(const uint16_t* q, const uint16_t* kc, const uint16
                              uint16_t* out, int T, int H, int G, int hd, int max_seq, int pos0,
                              hipStream_t s)
 {
-    attn::FlashArgs a{q, kc, vc, out, T, H, G, max_seq, pos0, (float)(1.0 / sqrt((double)hd))};
-    const dim3 grid(H, (T + attn::kFlashQ - 1) / attn::kFlashQ);
+    const int nqb = (T + attn::kFlashQ - 1) / attn::kFlashQ;
+    attn::FlashArgs a{q, kc, vc, out, T, H, G, max_seq, pos0, nqb,
+                      (float)(1.4426950408889634 / sqrt((double)hd))};
+    const dim3 grid((H * nqb + attn::kXcds - 1) / attn::kXcds * attn::kXcds);
     if (hd == 128)
         hipLaunchKernelGGL(attn::flash_kernel<128>, grid, dim3(256), 0, s, a);
     else
