@@ -727,15 +727,6 @@ __device__ inline uint32_t pack_bf16x2(float lo, float hi)
     return (uint32_t)moe::f32_to_bf16(lo) | ((uint32_t)moe::f32_to_bf16(hi) << 16);
 }
 
-// Two fp32 -> packed bf16 by one hardware conversion (round to nearest even;
-// used on finite values only, where it equals f32_to_bf16)
-__device__ inline uint32_t cvt_pk_bf16(float lo, float hi)
-{
-    typedef float f32x2_v __attribute__((ext_vector_type(2)));
-    typedef __bf16 bf16x2_v __attribute__((ext_vector_type(2)));
-    const f32x2_v in = {lo, hi};
-    return __builtin_bit_cast(uint32_t, __builtin_convertvector(in, bf16x2_v));
-}
 
 // Three workgroups per CU (the register cap keeps 3 waves per SIMD; with
 // the staging loads all in flight the compiler would otherwise take 172
@@ -906,9 +897,9 @@ __global__ __launch_bounds__(256, 3) void flash_kernel(FlashArgs a)
 #pragma unroll
             for (int i = 0; i < 4; ++i) {
                 const float p0v = pv[kb * 8 + 2 * i], p1v = pv[kb * 8 + 2 * i + 1];
-                const uint32_t h = cvt_pk_bf16(p0v, p1v);
+                const uint32_t h = moe::cvt_pk_bf16(p0v, p1v);
                 bh[i] = h;
-                bl[i] = cvt_pk_bf16(p0v - __uint_as_float(h << 16), p1v - __uint_as_float(h & 0xFFFF0000u));
+                bl[i] = moe::cvt_pk_bf16(p0v - __uint_as_float(h << 16), p1v - __uint_as_float(h & 0xFFFF0000u));
             }
 #pragma unroll
             for (int b = 0; b < DB; ++b) {

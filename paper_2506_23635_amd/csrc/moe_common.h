@@ -66,11 +66,23 @@ __device__ inline uint16_t f32_to_bf16(float v)
     return (uint16_t)(u >> 16);
 }
 
-// silu(g) * u with an overflow-free logistic: for g << 0, exp(-g) -> inf and
-// g / inf -> -0, which is the limit.
+// Two fp32 -> packed bf16 (lo in the low half) by the hardware conversion:
+// round to nearest even, equal to f32_to_bf16 on every non-NaN input; a NaN
+// stays a NaN.
+__device__ inline uint32_t cvt_pk_bf16(float lo, float hi)
+{
+    typedef float f32x2_v __attribute__((ext_vector_type(2)));
+    typedef __bf16 bf16x2_v __attribute__((ext_vector_type(2)));
+    const f32x2_v in = {lo, hi};
+    return __builtin_bit_cast(uint32_t, __builtin_convertvector(in, bf16x2_v));
+}
+
+// silu(g) * u with an overflow-free logistic: for g << 0, exp(-g) -> inf,
+// 1 / inf -> 0 and g * 0 -> -0, which is the limit.  The reciprocal is the
+// hardware one (1 ulp): the result is rounded to bf16 next.
 __device__ inline float silu_mul(float g, float u)
 {
-    return g / (1.0f + __expf(-g)) * u;
+    return g * __builtin_amdgcn_rcpf(1.0f + __expf(-g)) * u;
 }
 
 __device__ inline f32x4_t mfma16x16x32(const u32x4_t a, const u32x4_t b, f32x4_t c)

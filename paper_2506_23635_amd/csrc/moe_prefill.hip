@@ -355,10 +355,10 @@ __device__ __forceinline__ void process_tile(const GemmArgs& a, int ft, int tt, 
 #pragma unroll
                 for (int g = 0; g < 2; ++g) {
                     const int feat = (int)(rt / 2) * 16 + 8 * g + 4 * half;
-                    uint32_t h01 = (uint32_t)f32_to_bf16(silu_mul(v[4 * g + 0], v[4 * g + 8])) |
-                                   ((uint32_t)f32_to_bf16(silu_mul(v[4 * g + 1], v[4 * g + 9])) << 16);
-                    uint32_t h23 = (uint32_t)f32_to_bf16(silu_mul(v[4 * g + 2], v[4 * g + 10])) |
-                                   ((uint32_t)f32_to_bf16(silu_mul(v[4 * g + 3], v[4 * g + 11])) << 16);
+                    const uint32_t h01 = cvt_pk_bf16(silu_mul(v[4 * g + 0], v[4 * g + 8]),
+                                                     silu_mul(v[4 * g + 1], v[4 * g + 9]));
+                    const uint32_t h23 = cvt_pk_bf16(silu_mul(v[4 * g + 2], v[4 * g + 10]),
+                                                     silu_mul(v[4 * g + 3], v[4 * g + 11]));
                     *reinterpret_cast<uint2*>(a.H + (int64_t)row * a.f + feat) = make_uint2(h01, h23);
                 }
             } else {
