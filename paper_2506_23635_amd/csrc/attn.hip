@@ -737,7 +737,10 @@ __global__ __launch_bounds__(256, 3) void flash_kernel(FlashArgs a)
     constexpr int KS = HD / 32;              // K steps of the score MFMAs
     constexpr int DB = HD / 16;              // 16-dim blocks of the output
     constexpr int KROW = HD + 8;             // padded K row in LDS (bf16)
-    constexpr int VROW = kFlashP + 8;        // padded V^T row (positions, bf16)
+    // padded V^T row (positions, bf16): 34 words, so the 8-byte reads of 16
+    // consecutive dims fall in distinct bank pairs (LDS bank conflicts 19.5 M
+    // -> 6.5 M cycles per launch at 72)
+    constexpr int VROW = kFlashP + 4;
     __shared__ __attribute__((aligned(16))) uint16_t ks[kFlashP * KROW];
     __shared__ __attribute__((aligned(16))) uint16_t vt[HD * VROW];
     // XCD-aware numbering: hardware hands block b to XCD b % 8, and each XCD
