@@ -50,9 +50,6 @@ __device__ inline u32x4_t ld16_nt(const void* p)
 
 __device__ inline u32x4_t ld16(const void* p) { return *reinterpret_cast<const u32x4_t*>(p); }
 
-// the fp32 value of bf16(v) (round to nearest even)
-__device__ inline float bf16_round(float v) { return __uint_as_float((uint32_t)moe::f32_to_bf16(v) << 16); }
-
 // The output projection, o = a Wo (fp32) and y = bf16(x + o), one
 // workgroup per 16 output features.
 struct GemvArgs {
@@ -726,7 +723,6 @@ __device__ inline uint32_t pack_bf16x2(float lo, float hi)
 {
     return (uint32_t)moe::f32_to_bf16(lo) | ((uint32_t)moe::f32_to_bf16(hi) << 16);
 }
-
 
 // Three workgroups per CU (the register cap keeps 3 waves per SIMD; with
 // the staging loads all in flight the compiler would otherwise take 172
