@@ -690,20 +690,22 @@ __global__ __launch_bounds__(256) void rope_kernel(RopeArgs a)
 }
 
 // flash_kernel: causal attention of T new tokens, one workgroup of 4 waves
-// per (query head j, block of 64 query tokens); wave w owns tokens
-// 16 w .. 16 w + 15 of the block, one per lane column.  Per step of 64
-// positions of head j's key/value head: K rows and V transposed (dims major)
-// go to LDS; the scores are computed transposed, S^T = K Q^T, with
-// v_mfma_f32_16x16x32_bf16 (A = 16 positions x 32 dims of K from LDS, B =
-// the wave's query rows), so lane l ends with the scores of token l%16 at
-// positions 4(l/16) + r of each 16-position block; the running maximum and
-// sum per token (two butterfly steps) rescale the output, and O^T += V^T P^T
-// takes the P values straight from those registers as the B operand (the
-// 8 positions of a lane's K group are {4g..4g+3, 16+4g..16+4g+3} of a
-// 32-position block, and the V^T operand is read from LDS in the same
-// order).  P enters the matrix cores as two bf16 terms, bf16(p) and
-// bf16(p - bf16(p)), which keep 16 significant bits; V is bf16 and every
-// product is exact in the fp32 accumulation.
+// per (query head j, block of 128 query tokens); wave w owns tokens
+// 32 w .. 32 w + 31 of the block, one per lane column (lanes l and l + 32
+// share token l % 32).  Per step of 64 positions of head j's key/value head:
+// K rows and V transposed (dims major) go to LDS; the scores are computed
+// transposed, S^T = K Q^T, with v_mfma_f32_32x32x16_bf16 (A = 32 positions x
+// 16 dims of K from LDS, B = the wave's query rows), so lane l ends with the
+// scores of token l % 32 at positions 8 g + 4 (l / 32) + r of each
+// 32-position block (register 4 g + r); the running maximum and sum per
+// token (one exchange between the lane pair) rescale the output, and
+// O^T += V^T P^T takes the P values straight from those registers as the B
+// operand: the 16-position K step s of a block takes registers g = 2 s,
+// 2 s + 1, i.e. positions 16 s + {4 h .. 4 h + 3, 8 + 4 h .. 8 + 4 h + 3}
+// for h = l / 32, and the V^T operand is read from LDS in the same order.
+// P enters the matrix cores as two bf16 terms, bf16(p) and bf16(p - bf16(p)),
+// which keep 16 significant bits; V is bf16 and every product is exact in
+// the fp32 accumulation.
 struct FlashArgs {
     const uint16_t* q;     // [T][H][HD] bf16, rotated
     const uint16_t* kc;    // this layer's K cache [G][max_seq][HD]
@@ -716,7 +718,7 @@ struct FlashArgs {
 
 constexpr int kXcds = 8;
 
-constexpr int kFlashQ = 64;     // query tokens per workgroup
+constexpr int kFlashQ = 128;    // query tokens per workgroup
 constexpr int kFlashP = 64;     // positions per step
 
 __device__ inline uint32_t pack_bf16x2(float lo, float hi)
@@ -724,18 +726,25 @@ __device__ inline uint32_t pack_bf16x2(float lo, float hi)
     return (uint32_t)moe::f32_to_bf16(lo) | ((uint32_t)moe::f32_to_bf16(hi) << 16);
 }
 
-// Three workgroups per CU (the register cap keeps 3 waves per SIMD; with
-// the staging loads all in flight the compiler would otherwise take 172
-// registers and leave room for 2).
-template <int HD>
-__global__ __launch_bounds__(256, 3) void flash_kernel(FlashArgs a)
+typedef __attribute__((__vector_size__(16 * sizeof(float)))) float f32x16_t;
+
+__device__ inline f32x16_t mfma32x32x16(const u32x4_t a, const u32x4_t b, f32x16_t c)
 {
-    constexpr int KS = HD / 32;              // K steps of the score MFMAs
-    constexpr int DB = HD / 16;              // 16-dim blocks of the output
+    return __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(moe::bf16x8_t, a),
+                                                   __builtin_bit_cast(moe::bf16x8_t, b), c, 0, 0, 0);
+}
+
+// Two workgroups per CU: 219 registers per lane at head_dim 128 (the output
+// block of 32 tokens x 128 dims alone takes 64), 2 waves per SIMD.
+template <int HD>
+__global__ __launch_bounds__(256, 2) void flash_kernel(FlashArgs a)
+{
+    constexpr int KQ = HD / 16;              // 16-dim K steps of the score MFMAs
+    constexpr int DB = HD / 32;              // 32-dim blocks of the output
     constexpr int KROW = HD + 8;             // padded K row in LDS (bf16)
-    // padded V^T row (positions, bf16): 34 words, so the 8-byte reads of 16
+    // padded V^T row (positions, bf16): 34 words, so the 8-byte reads of
     // consecutive dims fall in distinct bank pairs (LDS bank conflicts 19.5 M
-    // -> 6.5 M cycles per launch at 72)
+    // -> 6.5 M cycles per launch against 36 words)
     constexpr int VROW = kFlashP + 4;
     __shared__ __attribute__((aligned(16))) uint16_t ks[kFlashP * KROW];
     __shared__ __attribute__((aligned(16))) uint16_t vt[HD * VROW];
@@ -753,24 +762,24 @@ __global__ __launch_bounds__(256, 3) void flash_kernel(FlashArgs a)
     const int qb = a.nqb - 1 - rem / groups;
     const int j = kvh * groups + rem % groups;
     const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
-    const int c = lane & 15, grp = lane >> 4;
-    const int t_w0 = qb * kFlashQ + w * 16;             // the wave's first token
+    const int c = lane & 31, h = lane >> 5;
+    const int t_w0 = qb * kFlashQ + w * 32;             // the wave's first token
     const int t = t_w0 + c;                              // this lane's token
     const bool tok_ok = t < a.T;
     const int lim = a.pos0 + t;                          // its last position
     const u32x4_t zero = {0u, 0u, 0u, 0u};
-    u32x4_t qf[KS];
+    u32x4_t qf[KQ];
     {
-        const uint16_t* qrow = a.q + ((int64_t)(tok_ok ? t : 0) * a.H + j) * HD + grp * 8;
+        const uint16_t* qrow = a.q + ((int64_t)(tok_ok ? t : 0) * a.H + j) * HD + h * 8;
 #pragma unroll
-        for (int k = 0; k < KS; ++k) {
-            const u32x4_t v = ld16(qrow + k * 32);
+        for (int k = 0; k < KQ; ++k) {
+            const u32x4_t v = ld16(qrow + k * 16);
             qf[k] = tok_ok ? v : zero;
         }
     }
-    f32x4_t o[DB];
+    f32x16_t o[DB];
 #pragma unroll
-    for (int b = 0; b < DB; ++b) o[b] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+    for (int b = 0; b < DB; ++b) o[b] = f32x16_t{};
     float m = -INFINITY, l = 0.f;
     const int t_last = min(qb * kFlashQ + kFlashQ, a.T) - 1;
     const int n_pos = a.pos0 + t_last + 1;               // positions the block needs
@@ -826,57 +835,56 @@ __global__ __launch_bounds__(256, 3) void flash_kernel(FlashArgs a)
             }
         }
         __syncthreads();
-        // S^T for the 4 blocks of 16 positions
-        f32x4_t st[4];
+        // S^T = K Q^T for the two 32-position blocks: lane (c, h) ends with
+        // token c's scores at positions 32 pb + 8 g + 4 h + r (register 4 g + r)
+        f32x16_t st[2];
 #pragma unroll
-        for (int pb = 0; pb < 4; ++pb) {
-            st[pb] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+        for (int pb = 0; pb < 2; ++pb) {
+            st[pb] = f32x16_t{};
 #pragma unroll
-            for (int k = 0; k < KS; ++k) {
+            for (int k = 0; k < KQ; ++k) {
                 const u32x4_t kf =
-                    *reinterpret_cast<const u32x4_t*>(&ks[(pb * 16 + c) * KROW + k * 32 + grp * 8]);
-                st[pb] = moe::mfma16x16x32(kf, qf[k], st[pb]);
+                    *reinterpret_cast<const u32x4_t*>(&ks[(pb * 32 + c) * KROW + k * 16 + h * 8]);
+                st[pb] = mfma32x32x16(kf, qf[k], st[pb]);
             }
         }
         // scores in base 2 (s * scale * log2 e, so p = 2^(s2 - m2)); the
         // causal mask and the tokens past T only on the steps that need them
         // (wave-uniform: a step past the wave's first token's last position,
         // or a wave with tokens past T)
-        float sv[16];
+        float sv[32];
         float mx = -INFINITY;
-        if (p0 + kFlashP - 1 > a.pos0 + t_w0 || t_w0 + 15 >= a.T) {
+        if (p0 + kFlashP - 1 > a.pos0 + t_w0 || t_w0 + 31 >= a.T) {
 #pragma unroll
-            for (int pb = 0; pb < 4; ++pb)
+            for (int pb = 0; pb < 2; ++pb)
 #pragma unroll
-                for (int r = 0; r < 4; ++r) {
-                    const int pos = p0 + pb * 16 + 4 * grp + r;
-                    const float v = (tok_ok && pos <= lim) ? st[pb][r] * a.scale2 : -INFINITY;
-                    sv[pb * 4 + r] = v;
+                for (int i = 0; i < 16; ++i) {
+                    const int pos = p0 + pb * 32 + 8 * (i / 4) + 4 * h + (i % 4);
+                    const float v = (tok_ok && pos <= lim) ? st[pb][i] * a.scale2 : -INFINITY;
+                    sv[pb * 16 + i] = v;
                     mx = fmaxf(mx, v);
                 }
         } else {
 #pragma unroll
-            for (int pb = 0; pb < 4; ++pb)
+            for (int pb = 0; pb < 2; ++pb)
 #pragma unroll
-                for (int r = 0; r < 4; ++r) {
-                    sv[pb * 4 + r] = st[pb][r] * a.scale2;
-                    mx = fmaxf(mx, sv[pb * 4 + r]);
+                for (int i = 0; i < 16; ++i) {
+                    sv[pb * 16 + i] = st[pb][i] * a.scale2;
+                    mx = fmaxf(mx, sv[pb * 16 + i]);
                 }
         }
-        mx = fmaxf(mx, __shfl_xor(mx, 16, 64));
         mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
         const float mn = fmaxf(m, mx);
         // a token with every position masked so far (only tokens past T)
         // keeps mn = -inf: subtract 0 instead, so its p are 0, not NaN
         const float msub = mn == -INFINITY ? 0.f : mn;
         float ps = 0.f;
-        float pv[16];
+        float pv[32];
 #pragma unroll
-        for (int e = 0; e < 16; ++e) {
+        for (int e = 0; e < 32; ++e) {
             pv[e] = __builtin_amdgcn_exp2f(sv[e] - msub);
             ps += pv[e];
         }
-        ps += __shfl_xor(ps, 16, 64);
         ps += __shfl_xor(ps, 32, 64);
         // rescale the running sums only where a maximum moved (m == mn gives
         // the factor 1 exactly, so skipping it changes no bit)
@@ -888,37 +896,46 @@ __global__ __launch_bounds__(256, 3) void flash_kernel(FlashArgs a)
         }
         l += ps;
         m = mn;
-        // O^T += V^T P^T over the two 32-position K blocks, P as hi + lo:
+        // O^T += V^T P^T, four 16-position K steps: step (pb, s) takes the
+        // lane's registers 4 g + r for g = 2 s, 2 s + 1 of block pb, i.e.
+        // positions 32 pb + 16 s + {4 h .. 4 h + 3, 8 + 4 h .. 8 + 4 h + 3},
+        // and the V^T operand is read in the same order; P as hi + lo,
         // hi = bf16(p), lo = bf16(p - hi) (the subtraction is exact)
 #pragma unroll
-        for (int kb = 0; kb < 2; ++kb) {
-            u32x4_t bh, bl;
+        for (int pb = 0; pb < 2; ++pb)
 #pragma unroll
-            for (int i = 0; i < 4; ++i) {
-                const float p0v = pv[kb * 8 + 2 * i], p1v = pv[kb * 8 + 2 * i + 1];
-                const uint32_t h = moe::cvt_pk_bf16(p0v, p1v);
-                bh[i] = h;
-                bl[i] = moe::cvt_pk_bf16(p0v - __uint_as_float(h << 16), p1v - __uint_as_float(h & 0xFFFF0000u));
-            }
+            for (int sx = 0; sx < 2; ++sx) {
+                const float* pp = &pv[pb * 16 + sx * 8];
+                u32x4_t bh, bl;
 #pragma unroll
-            for (int b = 0; b < DB; ++b) {
-                const uint32_t* vr = vt32 + ((b * 16 + c) * VROW + kb * 32 + 4 * grp) / 2;
-                const uint2 v0 = *reinterpret_cast<const uint2*>(vr);
-                const uint2 v1 = *reinterpret_cast<const uint2*>(vr + 8);
-                const u32x4_t av = {v0.x, v0.y, v1.x, v1.y};
-                o[b] = moe::mfma16x16x32(av, bh, o[b]);
-                o[b] = moe::mfma16x16x32(av, bl, o[b]);
+                for (int i = 0; i < 4; ++i) {
+                    const uint32_t hw = moe::cvt_pk_bf16(pp[2 * i], pp[2 * i + 1]);
+                    bh[i] = hw;
+                    bl[i] = moe::cvt_pk_bf16(pp[2 * i] - __uint_as_float(hw << 16),
+                                             pp[2 * i + 1] - __uint_as_float(hw & 0xFFFF0000u));
+                }
+#pragma unroll
+                for (int b = 0; b < DB; ++b) {
+                    const uint32_t* vr = vt32 + ((b * 32 + c) * VROW + pb * 32 + sx * 16 + 4 * h) / 2;
+                    const uint2 v0 = *reinterpret_cast<const uint2*>(vr);
+                    const uint2 v1 = *reinterpret_cast<const uint2*>(vr + 4);
+                    const u32x4_t av = {v0.x, v0.y, v1.x, v1.y};
+                    o[b] = mfma32x32x16(av, bh, o[b]);
+                    o[b] = mfma32x32x16(av, bl, o[b]);
+                }
             }
-        }
     }
     if (!tok_ok) return;
-    // lane: dims 16 b + 4 grp + r of token t
+    // lane: dims 32 b + 8 g + 4 h + r of token t (register 4 g + r)
     const float inv = 1.0f / l;
-    uint16_t* dst = a.out + ((int64_t)t * a.H + j) * HD + 4 * grp;
+    uint16_t* dst = a.out + ((int64_t)t * a.H + j) * HD + 4 * h;
 #pragma unroll
     for (int b = 0; b < DB; ++b)
-        *reinterpret_cast<uint2*>(dst + b * 16) =
-            make_uint2(pack_bf16x2(o[b][0] * inv, o[b][1] * inv), pack_bf16x2(o[b][2] * inv, o[b][3] * inv));
+#pragma unroll
+        for (int g = 0; g < 4; ++g)
+            *reinterpret_cast<uint2*>(dst + b * 32 + 8 * g) =
+                make_uint2(pack_bf16x2(o[b][4 * g] * inv, o[b][4 * g + 1] * inv),
+                           pack_bf16x2(o[b][4 * g + 2] * inv, o[b][4 * g + 3] * inv));
 }
 
 // y = bf16(x + o), 8 elements per thread
