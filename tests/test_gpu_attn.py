@@ -248,12 +248,14 @@ def test_projection_shapes(torch_mod, d, H, G, hd, T):
         case.close()
 
 
-@pytest.mark.parametrize("T,pos0", [(17, 0), (64, 37), (100, 200), (130, 0)])
+@pytest.mark.parametrize("T,pos0", [(17, 0), (64, 37), (100, 200), (130, 0), (171, 341)])
 def test_prefill_small_block(torch_mod, T, pos0):
     """More than 16 new tokens: the prefill path (projection GEMMs, rotation
     and cache append, causal attention on the matrix cores), every stage
-    per element; T spans partial 64-token query blocks and 256-row GEMM
-    tiles, pos0 a cached prefix or none."""
+    per element; T spans partial 128-token query blocks, partial 64-position
+    steps and 256-row GEMM tiles, pos0 a cached prefix or none; the last
+    case ends exactly at the cache's last position (pos0 + T = max_seq =
+    512), so the last query block's K/V loads reach the end of the cache."""
     torch = torch_mod
     wl = TINY.with_(T=T, pos0=pos0)
     case = Case(torch, wl, max_tokens=256)
@@ -273,7 +275,8 @@ def test_prefill_dbrx_block(torch_mod, T, pos0):
     positions, and the whole 2048-token prompt of the long-prompt workload
     from an empty cache.  Every stage per element except the attention
     bound, which is checked on sampled tokens (first and last of every
-    64-token query block and a seeded sample)."""
+    64-token span, so of every 128-token query block, and a seeded
+    sample)."""
     torch = torch_mod
     wl = DBRX.with_(T=T, pos0=pos0)
     case = Case(torch, wl, max_tokens=2048, on_device=True)
