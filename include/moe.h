@@ -326,6 +326,15 @@ MOE_API const char *moe_status_string(moe_status s);
 MOE_API moe_status moe_diag_stream_read(const void *src, uint64_t bytes, uint32_t *out,
                                         moe_stream_t stream);
 
+/* Diagnostics: dst[i] = bf16(src[i]) for i < n by the hardware conversion
+ * that the grouped GEMM's gate/up epilogue applies to H (R5: round to
+ * nearest even; a NaN stays a NaN), so that a test can hold it against the
+ * integer rounding on every fp32 pattern.  src fp32 [n] and dst bf16 [n],
+ * device memory; src 8-byte and dst 4-byte aligned and n even, else
+ * MOE_E_ARG (nothing enqueued); n == 0 enqueues nothing.  Enqueued on
+ * stream; allocates nothing. */
+MOE_API moe_status moe_diag_bf16(const float *src, uint16_t *dst, uint64_t n, moe_stream_t stream);
+
 #ifdef __cplusplus
 }
 #endif

@@ -29,7 +29,7 @@ EXPORTED = ["moe_weight_bytes", "moe_workspace_bytes", "moe_workspace_map", "moe
             "moe_forward_stack", "moe_forward_layers", "moe_forward_residual",
             "moe_intermediates", "moe_profile_enable", "moe_profile_read",
             "moe_profile_gemm_timeline", "moe_destroy",
-            "moe_last_error", "moe_status_string", "moe_diag_stream_read",
+            "moe_last_error", "moe_status_string", "moe_diag_stream_read", "moe_diag_bf16",
             # include/attn.h
             "attn_weight_bytes", "attn_cache_bytes", "attn_workspace_bytes", "attn_init",
             "attn_load_layer", "attn_load_post_norm", "attn_forward", "attn_forward_norm",
@@ -114,6 +114,7 @@ def lib():
         L.moe_status_string.argtypes = [ctypes.c_int]
         L.moe_status_string.restype = ctypes.c_char_p
         L.moe_diag_stream_read.argtypes = [P, ctypes.c_uint64, P, P]
+        L.moe_diag_bf16.argtypes = [P, P, ctypes.c_uint64, P]
         acfg = ctypes.POINTER(AttnConfig)
         for fn in ("attn_weight_bytes", "attn_cache_bytes", "attn_workspace_bytes"):
             getattr(L, fn).argtypes = [acfg]
@@ -138,7 +139,8 @@ def lib():
                    "moe_forward_static", "moe_forward_stack", "moe_forward_layers",
                    "moe_forward_residual",
                    "moe_intermediates", "moe_profile_enable",
-                   "moe_profile_read", "moe_profile_gemm_timeline", "moe_diag_stream_read"):
+                   "moe_profile_read", "moe_profile_gemm_timeline", "moe_diag_stream_read",
+                   "moe_diag_bf16"):
             getattr(L, fn).restype = ctypes.c_int
         _lib = L
     return _lib
@@ -222,6 +224,14 @@ def moe_diag_stream_read(src_ptr, nbytes, out_ptr, stream=0):
     XOR of its words to the 4 uint32 at out_ptr + 16 b (device pointers; out
     holds DIAG_MAX_WG x 4 uint32, zeroed by the caller; see include/moe.h)."""
     st = lib().moe_diag_stream_read(src_ptr, nbytes, out_ptr, stream)
+    if st != MOE_OK:
+        raise MoeError(st, lib().moe_status_string(st).decode())
+
+
+def moe_diag_bf16(src_ptr, dst_ptr, n, stream=0):
+    """dst[i] = bf16(src[i]), i < n, by the gate/up epilogue's hardware
+    conversion (device pointers; see include/moe.h)."""
+    st = lib().moe_diag_bf16(src_ptr, dst_ptr, n, stream)
     if st != MOE_OK:
         raise MoeError(st, lib().moe_status_string(st).decode())
 

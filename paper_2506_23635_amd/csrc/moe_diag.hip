@@ -1,7 +1,11 @@
 // moe_diag.hip -- diagnostics beside the layer: a plain streaming read of a
 // device buffer, the achievable HBM read rate that the layer's weight
-// streams are compared with (the spec peak is 8 TB/s).
+// streams are compared with (the spec peak is 8 TB/s); and the hardware
+// fp32 -> bf16 conversion of the grouped GEMM's gate/up epilogue, applied to
+// a caller's array so that it can be checked against round-to-nearest-even
+// on every fp32 pattern.
 //
+// The streaming read:
 // Each workgroup reads one contiguous chunk of the buffer: per iteration
 // its 256 lanes load 8 x 4 KiB of consecutive 16-byte words (1 KiB per
 // wave-load, nontemporal, eight loads in flight per lane), and XOR them; the
@@ -46,7 +50,32 @@ __global__ __launch_bounds__(kDiagThreads) void stream_read_kernel(const u32x4_t
     }
 }
 
+// y[i] = bf16(x[i]) by cvt_pk_bf16, two elements per thread, grid-stride
+__global__ __launch_bounds__(kDiagThreads) void bf16_convert_kernel(const float2* __restrict__ x,
+                                                                    uint32_t* __restrict__ y,
+                                                                    uint64_t n_pairs)
+{
+    for (uint64_t i = (uint64_t)blockIdx.x * kDiagThreads + threadIdx.x; i < n_pairs;
+         i += (uint64_t)gridDim.x * kDiagThreads) {
+        const float2 v = x[i];
+        y[i] = cvt_pk_bf16(v.x, v.y);
+    }
+}
+
 }  // namespace moe
+
+extern "C" moe_status moe_diag_bf16(const float* src, uint16_t* dst, uint64_t n, moe_stream_t stream)
+{
+    if (!src || !dst || ((uintptr_t)src & 7) || ((uintptr_t)dst & 3) || n % 2) return MOE_E_ARG;
+    if (n == 0) return MOE_OK;
+    const uint64_t n_pairs = n / 2;
+    const uint64_t want = (n_pairs + moe::kDiagThreads - 1) / moe::kDiagThreads;
+    const int grid = (int)(want < 8192 ? want : 8192);
+    hipLaunchKernelGGL(moe::bf16_convert_kernel, dim3(grid), dim3(moe::kDiagThreads), 0,
+                       static_cast<hipStream_t>(stream), reinterpret_cast<const float2*>(src),
+                       reinterpret_cast<uint32_t*>(dst), n_pairs);
+    return hipGetLastError() == hipSuccess ? MOE_OK : MOE_E_HIP;
+}
 
 extern "C" moe_status moe_diag_stream_read(const void* src, uint64_t bytes, uint32_t* out,
                                            moe_stream_t stream)

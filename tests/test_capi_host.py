@@ -191,6 +191,17 @@ def test_diag_stream_read_rejects_bad_arguments():
     assert lib.moe_diag_stream_read(aligned, 0, aligned, None) == moe.MOE_OK
 
 
+def test_diag_bf16_rejects_bad_arguments():
+    lib = moe.lib()
+    aligned = 1 << 20
+    assert lib.moe_diag_bf16(None, aligned, 2, None) == E_ARG
+    assert lib.moe_diag_bf16(aligned, None, 2, None) == E_ARG
+    assert lib.moe_diag_bf16(aligned + 4, aligned, 2, None) == E_ARG
+    assert lib.moe_diag_bf16(aligned, aligned + 2, 2, None) == E_ARG
+    assert lib.moe_diag_bf16(aligned, aligned, 3, None) == E_ARG
+    assert lib.moe_diag_bf16(aligned, aligned, 0, None) == moe.MOE_OK
+
+
 def test_binding_checks_tensors_before_the_abi():
     """The C-ABI takes plain pointers and cannot see sizes, so the binding
     rejects a tensor of the wrong dtype, a strided view, a tensor on another

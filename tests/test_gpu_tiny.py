@@ -654,3 +654,29 @@ def test_diag_stream_read_reads_every_word_once(torch_mod, nbytes):
     expect = np.bitwise_xor.reduce(words, axis=0)
     got = np.bitwise_xor.reduce(out.cpu().numpy().view(np.uint32).reshape(-1, 4), axis=0)
     assert np.array_equal(got, expect)
+
+
+def test_diag_bf16_is_round_to_nearest_even_on_every_fp32_pattern(torch_mod):
+    """The hardware fp32 -> bf16 conversion that the grouped GEMM's gate/up
+    epilogue applies to H, over all 2^32 fp32 bit patterns (16 chunks of
+    2^28): equal, bit for bit, to the integer round-to-nearest-even
+    (u + 0x7FFF + ((u >> 16) & 1)) >> 16 on every non-NaN input, and a NaN
+    for every NaN input."""
+    torch = torch_mod
+    n = 1 << 28
+    s = torch.cuda.current_stream().cuda_stream
+    out = torch.empty(n, dtype=torch.int16, device="cuda")
+    for c in range(16):
+        lo = -(1 << 31) + c * n
+        bits = torch.arange(lo, lo + n, dtype=torch.int32, device="cuda")
+        moe.moe_diag_bf16(bits.data_ptr(), out.data_ptr(), n, s)
+        u = bits.to(torch.int64) & 0xFFFFFFFF
+        want = ((u + 0x7FFF + ((u >> 16) & 1)) >> 16) & 0xFFFF
+        got = out.to(torch.int64) & 0xFFFF
+        nan_in = ((u & 0x7F800000) == 0x7F800000) & ((u & 0x7FFFFF) != 0)
+        nan_out = ((got & 0x7F80) == 0x7F80) & ((got & 0x7F) != 0)
+        assert torch.equal(nan_in, nan_in & nan_out), f"chunk {c}: a NaN input gave a non-NaN"
+        bad = (~nan_in) & (got != want)
+        assert int(bad.sum()) == 0, f"chunk {c}: {int(bad.sum())} mismatches"
+        del bits, u, want, got, nan_in, nan_out, bad
+    torch.cuda.synchronize()
