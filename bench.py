@@ -1125,6 +1125,13 @@ def main():
                         "collective_latency_s_assumed": 20e-6, "link_gbs_assumed": 150.0},
              "predictions": perf_model.mi355x_predictions(bw_meas, tf_meas),
              "placements": placement.mi355x_placement_predictions(bw_meas, tf_meas)}
+    if decoder:
+        # the one-GPU prediction beside the measured 40-layer decoder token
+        # (the model leaves out the per-kernel fixed costs)
+        pred = model["predictions"]["1"]["ms_per_token"]
+        model["measured_1gpu"] = {"ms_per_token": decoder["ms_per_token"],
+                                  "predicted_ms_per_token": pred,
+                                  "measured_over_predicted": decoder["ms_per_token"] / pred}
 
     out = {
         "metric": METRIC,
