@@ -248,6 +248,26 @@ def test_projection_shapes(torch_mod, d, H, G, hd, T):
         case.close()
 
 
+@pytest.mark.parametrize("d,H,G,hd,T,pos0", [(2048, 32, 8, 64, 40, 70), (1024, 8, 8, 128, 150, 30),
+                                               (1024, 8, 1, 128, 150, 30), (4096, 32, 4, 128, 200, 0)])
+def test_prefill_shapes(torch_mod, d, H, G, hd, T, pos0):
+    """The prefill path on other head layouts, every stage per element:
+    head_dim 64 at four query heads per key/value head, one query head per
+    key/value head (multi-head attention) and one key/value head for all
+    (multi-query), and eight per head at d 4096; the causal attention's
+    workgroup numbering then maps 1, 4 or 8 query heads to a key/value head."""
+    torch = torch_mod
+    wl = TINY.with_(d=d, n_heads=H, n_kv=G, hd=hd, T=T, pos0=pos0)
+    case = Case(torch, wl, max_tokens=256)
+    try:
+        x = wl.x()
+        y = case.forward(x, pos0)
+        kc, vc = case.cache()
+        check_block(case, x, pos0, y, case.layer.intermediates(T), kc, vc)
+    finally:
+        case.close()
+
+
 @pytest.mark.parametrize("T,pos0", [(17, 0), (64, 37), (100, 200), (130, 0), (171, 341)])
 def test_prefill_small_block(torch_mod, T, pos0):
     """More than 16 new tokens: the prefill path (projection GEMMs, rotation
